@@ -1,0 +1,298 @@
+"""Plain fp64 CPU oracle for cluster-level sparse prefill (Similarity Chunk Rolling, SCR).
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline``
+leg of ``bench.py`` may import or call this module. The product path (the HIP library and its
+Python binding) never does, and this module never imports the product path.
+
+It follows the paper's statement of the method, step by step, in float64, with no blocking,
+fusion or reordering beyond what the definitions say. Citations name the paper's sections and
+equations (equation numbers in source order):
+
+* Sec. 3.1, two-level chunked prefill: an outer chunk's queries are split into M = ceil(l / L)
+  sub-chunks, the last one possibly short.
+* Sec. 3.2, Definition 1 (Eqs. 2-4): selective sparse attention restricts the softmax of scaled
+  dot-product attention (Eq. 1) to a selected subset of the cache, chosen by a selection function
+  over all heads.
+* Sec. 4.1, Eq. 6: the sub-chunk fingerprint is the mean of the sub-chunk's multi-head queries;
+  its head-h slice is the per-head mean.
+* Sec. 5.1.3, Eq. 9: one selection per cluster, driven by the anchor (first sub-chunk)
+  fingerprint, shared by every member.
+* Sec. 5.1.3, "selection function instantiation": head soft-voting -- per-head dot scores,
+  softmax per head, sum over heads, top-k.
+* Sec. 5.1.3, Eq. 10: cluster attention over three key groups (the shared top-k set, the
+  attention sinks, and a local window widened to span the whole cluster) under a causal mask.
+* Algorithm 2: per cluster, select -> augment with sink and local -> attend -> write.
+
+Readings where the paper is silent (block-level selection, the representative key, the
+candidate set, local-window geometry, tie-break), all named R-numbers below, are listed with
+their reasons in the design notes:
+
+  R1  selection unit is a KV block of B tokens (blocks, not single tokens, are scored)
+  R2  a block's representative key is the arithmetic mean of its keys, per KV head
+  R4  the cluster query is the anchor fingerprint: mean of the first sub-chunk's query rows
+  R5  selection logits are v . k_rep times ``score_scale`` (default 1.0, the literal text)
+  R6  query head h reads KV head floor(h * Hkv / Hq)
+  R7  one index set per cluster, shared by all heads (scores summed over every query head)
+  R8  the soft-voting softmax runs over the candidate blocks only
+  R9  candidates are the blocks strictly between the sink blocks and the local window
+  R10 local window starts at lo = max(0, min(s, e - W)), rounded down to a block: it spans the
+      whole cluster and at least W tokens before the cluster end
+  R11 the sink is the first ceil(S / B) whole blocks, clipped to the blocks before the window
+  R12 top-k order is (score descending, block index ascending); fewer candidates than k selects
+      them all; the selection is emitted in ascending block order
+  R13 causal: a key is visible to a query iff its position is <= the query's position
+  R14 attention scale 1/sqrt(d_h) (Eqs. 1, 10) unless given
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+__all__ = [
+    "ClusterGeometry",
+    "geometry",
+    "bf16_to_f64",
+    "logical_kv",
+    "rep_keys",
+    "anchor_fingerprint",
+    "block_logits",
+    "soft_vote",
+    "select_topk",
+    "key_positions",
+    "attention_rows",
+    "cluster_attention",
+    "prefill",
+    "retrieval_calls",
+]
+
+
+def bf16_to_f64(u16) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> float64, exactly."""
+    u32 = np.asarray(u16, dtype=np.uint16).astype(np.uint32) << 16
+    return u32.view(np.float32).astype(np.float64)
+
+
+@dataclasses.dataclass(frozen=True)
+class ClusterGeometry:
+    """Token geometry of one cluster (all positions are token indices, half-open ranges)."""
+
+    s: int            # first query row of the cluster
+    e: int            # one past the last query row
+    anchor_end: int   # the anchor sub-chunk is rows [s, anchor_end)
+    lo_blk: int       # local window starts at token lo_blk * B
+    sink_blk: int     # ceil(S / B): blocks reserved for the sink
+    sink_eff: int     # sink blocks actually used: [0, sink_eff)
+    n_cand: int       # candidate blocks are [sink_blk, sink_blk + n_cand)
+    sel_cnt: int      # min(k, n_cand)
+
+
+def geometry(n_tokens: int, sub_chunk: int, block_size: int, sink_tokens: int, local_window: int,
+             top_k: int, cluster_start) -> list[ClusterGeometry]:
+    """Per-cluster geometry (Sec. 3.1 sub-chunks; Sec. 5.1.3 and Eq. 10 key groups; R9-R12).
+
+    ``cluster_start`` holds sub-chunk indices: cluster j covers sub-chunks
+    [cluster_start[j], cluster_start[j+1]).
+    """
+    L, B, S, W, k = sub_chunk, block_size, sink_tokens, local_window, top_k
+    M = -(-n_tokens // L)
+    cs = [int(x) for x in cluster_start]
+    if len(cs) < 2 or cs[0] != 0 or cs[-1] != M or any(b <= a for a, b in zip(cs, cs[1:])):
+        raise ValueError("cluster_start must rise strictly from 0 to ceil(n_tokens / sub_chunk)")
+    out = []
+    sink_blk = -(-S // B)
+    for j in range(len(cs) - 1):
+        s = cs[j] * L
+        e = min(cs[j + 1] * L, n_tokens)
+        anchor_end = min(s + L, e)
+        lo = max(0, min(s, e - W))
+        lo_blk = lo // B
+        sink_eff = min(sink_blk, lo_blk)
+        n_cand = max(0, lo_blk - sink_blk)
+        out.append(ClusterGeometry(s, e, anchor_end, lo_blk, sink_blk, sink_eff, n_cand, min(k, n_cand)))
+    return out
+
+
+def retrieval_calls(n_clusters_per_layer) -> int:
+    """One selection call per cluster per layer, degenerate clusters included (Sec. 5.1.2)."""
+    return int(sum(int(n) for n in n_clusters_per_layer))
+
+
+def logical_kv(pages, block_table, blocks) -> np.ndarray:
+    """Keys (or values) of the given logical blocks as float64 [len(blocks) * B, Hkv, d].
+
+    ``pages`` is the paged cache [n_pages, Hkv, B, d]; ``block_table[b]`` is the page holding
+    logical block b.
+    """
+    blocks = np.asarray(blocks, dtype=np.int64)
+    if blocks.size == 0:
+        return np.zeros((0, pages.shape[1], pages.shape[3]), dtype=np.float64)
+    phys = np.asarray(block_table)[blocks]
+    x = bf16_to_f64(pages[phys])                   # [nb, Hkv, B, d]
+    return x.transpose(0, 2, 1, 3).reshape(-1, pages.shape[1], pages.shape[3])
+
+
+def rep_keys(k_pages, block_table, n_tokens: int, block_size: int, blocks=None) -> np.ndarray:
+    """R2: k_rep[b][g] = mean of K[t][g] over the valid tokens t of block b. [n, Hkv, d] fp64."""
+    n_blocks = -(-n_tokens // block_size)
+    blocks = np.arange(n_blocks) if blocks is None else np.asarray(blocks)
+    Hkv, d = k_pages.shape[1], k_pages.shape[3]
+    out = np.empty((len(blocks), Hkv, d), dtype=np.float64)
+    for i, b in enumerate(blocks):
+        n_valid = min(block_size, n_tokens - int(b) * block_size)
+        keys = bf16_to_f64(k_pages[int(block_table[int(b)]), :, :n_valid, :])   # [Hkv, n_valid, d]
+        out[i] = keys.sum(axis=1) / n_valid
+    return out
+
+
+def anchor_fingerprint(q, s: int, anchor_end: int) -> np.ndarray:
+    """Eq. 6 on the anchor sub-chunk (Eq. 9): v[h] = mean over rows p in [s, anchor_end) of q[p][h].
+
+    ``q`` is [N, Hq, d] bf16 bits (or any array indexable by row). Returns [Hq, d] fp64.
+    """
+    rows = bf16_to_f64(q[s:anchor_end])
+    return rows.sum(axis=0) / (anchor_end - s)
+
+
+def block_logits(v, k_rep_cand, num_kv_heads: int, score_scale: float = 1.0) -> np.ndarray:
+    """Per-head dot scores of the selection function (R5, R6): x[h][b] = sigma * v[h] . k_rep[b][g(h)].
+
+    ``v`` [Hq, d]; ``k_rep_cand`` [n_cand, Hkv, d]. Returns [Hq, n_cand].
+    """
+    Hq = v.shape[0]
+    x = np.empty((Hq, k_rep_cand.shape[0]), dtype=np.float64)
+    for h in range(Hq):
+        g = (h * num_kv_heads) // Hq
+        x[h] = score_scale * (k_rep_cand[:, g, :] @ v[h])
+    return x
+
+
+def soft_vote(x) -> np.ndarray:
+    """Head soft-voting (Sec. 5.1.3): softmax over candidates per head, then sum over heads (R7, R8)."""
+    if x.shape[1] == 0:
+        return np.zeros(0, dtype=np.float64)
+    m = x.max(axis=1, keepdims=True)
+    ex = np.exp(x - m)
+    p = ex / ex.sum(axis=1, keepdims=True)
+    return p.sum(axis=0)
+
+
+def select_topk(scores, first_block: int, k: int):
+    """R12: the top min(k, n) candidates by (score descending, block index ascending).
+
+    Returns (selected block indices in ascending order, margin), where the margin is the gap
+    between the k-th and (k+1)-th score in that order (+inf when every candidate is selected).
+    """
+    n = len(scores)
+    idx = np.arange(first_block, first_block + n)
+    order = np.lexsort((idx, -np.asarray(scores)))        # primary key: -score; ties: index
+    cnt = min(k, n)
+    sel = np.sort(idx[order[:cnt]])
+    margin = math.inf if n <= k else float(scores[order[cnt - 1]] - scores[order[cnt]]) if cnt > 0 else math.inf
+    return sel.astype(np.int64), margin
+
+
+def key_positions(geo: ClusterGeometry, sel, p: int, block_size: int) -> np.ndarray:
+    """Eq. 10 key set of query row p: sink blocks, the shared selected blocks, and the local
+    window [lo_blk * B, p] (causal, R13). The three groups are disjoint by construction (R9)."""
+    B = block_size
+    sink = np.arange(0, geo.sink_eff * B)
+    chosen = (np.asarray(sel, dtype=np.int64)[:, None] * B + np.arange(B)[None, :]).reshape(-1)
+    local = np.arange(geo.lo_blk * B, p + 1)
+    return np.concatenate([sink, chosen, local])
+
+
+def attention_rows(q, k_pages, v_pages, block_table, geo: ClusterGeometry, sel, rows, block_size: int,
+                   softmax_scale: float | None = None, heads=None) -> np.ndarray:
+    """Eq. 10 for the query rows ``rows`` (all inside the cluster), fp64: [len(rows), len(heads), d].
+
+    Every row attends to its own key set (``key_positions``); the softmax subtracts the row max.
+    ``sel`` may be any index set (the oracle's own or one under test).
+    """
+    rows = np.asarray(rows, dtype=np.int64)
+    Hq, d = q.shape[1], q.shape[2]
+    Hkv = k_pages.shape[1]
+    heads = np.arange(Hq) if heads is None else np.asarray(heads)
+    scale = 1.0 / math.sqrt(d) if not softmax_scale else float(softmax_scale)
+    B = block_size
+    if len(rows) and (rows.min() < geo.s or rows.max() >= geo.e):
+        raise ValueError("rows outside the cluster")
+    out = np.empty((len(rows), len(heads), d), dtype=np.float64)
+    if len(rows) == 0:
+        return out
+    # Logical keys/values of every block any requested row can see.
+    p_max = int(rows.max())
+    blocks = np.concatenate([np.arange(geo.sink_eff), np.asarray(sel, dtype=np.int64),
+                             np.arange(geo.lo_blk, p_max // B + 1)]).astype(np.int64)
+    Kx = logical_kv(k_pages, block_table, blocks)        # [nk, Hkv, d]
+    Vx = logical_kv(v_pages, block_table, blocks)
+    pos = (blocks[:, None] * B + np.arange(B)[None, :]).reshape(-1)
+    qx = bf16_to_f64(q[rows])                            # [nr, Hq, d]
+    # Mask from the key-set definition: key t is visible to row p iff t is in Kset(p).
+    n_fixed = (geo.sink_eff + len(sel)) * B
+    visible = np.ones((len(rows), len(pos)), dtype=bool)
+    visible[:, n_fixed:] = pos[None, n_fixed:] <= rows[:, None]
+    for hi, h in enumerate(heads):
+        g = (int(h) * Hkv) // Hq
+        s = (qx[:, h, :] @ Kx[:, g, :].T) * scale         # [nr, nk]
+        s = np.where(visible, s, -np.inf)
+        m = s.max(axis=1, keepdims=True)
+        w = np.exp(s - m)
+        out[:, hi, :] = (w @ Vx[:, g, :]) / w.sum(axis=1, keepdims=True)
+    return out
+
+
+def cluster_attention(q, k_pages, v_pages, block_table, geo, sel, block_size, softmax_scale=None,
+                      row_chunk: int = 512) -> np.ndarray:
+    """Eq. 10 over every row of the cluster: [e - s, Hq, d] fp64."""
+    out = np.empty((geo.e - geo.s, q.shape[1], q.shape[2]), dtype=np.float64)
+    for r0 in range(geo.s, geo.e, row_chunk):
+        rows = np.arange(r0, min(r0 + row_chunk, geo.e))
+        out[r0 - geo.s: r0 - geo.s + len(rows)] = attention_rows(
+            q, k_pages, v_pages, block_table, geo, sel, rows, block_size, softmax_scale)
+    return out
+
+
+def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, block_size: int,
+            top_k: int, sink_tokens: int, local_window: int, cluster_start, score_scale: float = 1.0,
+            softmax_scale: float | None = None, with_output: bool = True, external_sel=None) -> dict:
+    """Algorithm 2 for one layer with a given cluster assignment.
+
+    For each cluster: anchor fingerprint -> block logits -> soft-voting scores -> top-k
+    (selection) -> attention of every row over sink + selected + local keys.
+    ``external_sel`` (list of index arrays) replaces the oracle's own selection in the attention
+    step, so attention can be checked under another selection.
+    Returns a dict with geometry, k_rep, fingerprints, scores, selections, margins, output.
+    """
+    geo = geometry(n_tokens, sub_chunk, block_size, sink_tokens, local_window, top_k, cluster_start)
+    k_rep = rep_keys(k_pages, block_table, n_tokens, block_size)
+    Hkv = k_pages.shape[1]
+    fps, scores, sels, margins = [], [], [], []
+    for g in geo:
+        v = anchor_fingerprint(q, g.s, g.anchor_end)
+        x = block_logits(v, k_rep[g.sink_blk:g.sink_blk + g.n_cand], Hkv, score_scale)
+        sc = soft_vote(x)
+        sel, margin = select_topk(sc, g.sink_blk, top_k)
+        fps.append(v)
+        scores.append(sc)
+        sels.append(sel)
+        margins.append(margin)
+    out = None
+    if with_output:
+        out = np.empty((n_tokens, q.shape[1], q.shape[2]), dtype=np.float64)
+        for j, g in enumerate(geo):
+            sel = sels[j] if external_sel is None else np.asarray(external_sel[j], dtype=np.int64)
+            out[g.s:g.e] = cluster_attention(q, k_pages, v_pages, block_table, g, sel, block_size,
+                                             softmax_scale)
+    return {
+        "geometry": geo,
+        "k_rep": k_rep,
+        "fingerprints": fps,
+        "scores": scores,
+        "selections": sels,
+        "margins": margins,
+        "output": out,
+        "retrieval_calls": len(geo),
+        "degenerate": sum(1 for g in geo if g.n_cand <= top_k),
+    }

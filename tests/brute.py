@@ -1,0 +1,139 @@
+"""Brute-force references used to pin the oracle on tiny inputs.
+
+Written separately from the oracle and in a different style: token-level loops, explicit
+position sets, an explicit N x N visibility mask, and exhaustive subset enumeration. Nothing here
+imports the oracle or the HIP path.
+
+* Selection (paper Sec. 5.1.3, Eq. 9 and head soft-voting): a block's logit for head h is the
+  average over the block's tokens t and the anchor rows p of q[p][h] . k[t][g(h)] -- by bilinearity
+  this equals the anchor-mean query dotted with the block-mean key. Softmax per head over the
+  candidate blocks, summed over heads; the chosen set is the k-subset with the largest total score,
+  ties broken toward the lexicographically smallest sorted index tuple.
+* Attention (Eq. 10): dense softmax over all N keys under a boolean mask built from the three key
+  groups (sink, selected blocks, cluster-spanning local window) and the causal rule.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+
+
+def widen(u16):
+    return (np.asarray(u16, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def unpage(pages, block_table):
+    """[n_pages, Hkv, B, d] bf16 bits + table -> logical fp64 [n_blocks * B, Hkv, d]."""
+    nb = len(block_table)
+    Hkv, B, d = pages.shape[1], pages.shape[2], pages.shape[3]
+    out = np.empty((nb * B, Hkv, d))
+    for b in range(nb):
+        blk = widen(pages[int(block_table[b])])        # [Hkv, B, d]
+        for t in range(B):
+            out[b * B + t] = blk[:, t, :]
+    return out
+
+
+def cluster_layout(n_tokens, L, B, S, W, cluster_start):
+    """(s, e, anchor_end, lo_blk, sink_eff, cand list) per cluster, from the definitions."""
+    res = []
+    for j in range(len(cluster_start) - 1):
+        s = int(cluster_start[j]) * L
+        e = min(int(cluster_start[j + 1]) * L, n_tokens)
+        anchor_end = min(s + L, e)
+        # the local window covers the whole cluster and at least W tokens ending at e
+        lo = s if e - s >= W else max(0, e - W)
+        lo_blk = lo // B
+        sink_blocks = [b for b in range(math.ceil(S / B)) if b < lo_blk]
+        cand = [b for b in range(lo_blk) if b >= math.ceil(S / B)]
+        res.append((s, e, anchor_end, lo_blk, len(sink_blocks), cand))
+    return res
+
+
+def brute_scores(q, K, anchor_rows, cand, B, Hkv, score_scale=1.0):
+    """Soft-voting score of every candidate block, by explicit loops. q fp64 [N, Hq, d], K fp64
+    logical [N, Hkv, d]."""
+    Hq = q.shape[1]
+    G = Hq // Hkv
+    total = {b: 0.0 for b in cand}
+    for h in range(Hq):
+        g = h // G
+        logits = {}
+        for b in cand:
+            acc = 0.0
+            for p in anchor_rows:
+                acc += float(np.dot(K[b * B:(b + 1) * B, g, :], q[p, h, :]).sum())
+            logits[b] = score_scale * acc / (len(anchor_rows) * B)
+        if not logits:
+            continue
+        mx = max(logits.values())
+        den = sum(math.exp(x - mx) for x in logits.values())
+        for b in cand:
+            total[b] += math.exp(logits[b] - mx) / den
+    return total
+
+
+def brute_select(scores: dict, k: int, rel_tie: float = 1e-12):
+    cand = sorted(scores)
+    if len(cand) <= k:
+        return tuple(cand)
+    best, best_sum = None, -math.inf
+    for combo in itertools.combinations(cand, k):     # generated in lexicographic order
+        ssum = sum(scores[b] for b in combo)
+        if best is None or ssum > best_sum + rel_tie * max(1.0, abs(best_sum)):
+            best, best_sum = combo, ssum
+    return best
+
+
+def visibility_mask(n_tokens, layout, selections, B):
+    """Explicit N x N mask: vis[p][t] is True iff key t is in query p's key set."""
+    vis = np.zeros((n_tokens, n_tokens), dtype=bool)
+    for (s, e, _a, lo_blk, sink_eff, _c), sel in zip(layout, selections):
+        allowed = set(range(sink_eff * B))
+        for b in sel:
+            allowed.update(range(b * B, (b + 1) * B))
+        for p in range(s, e):
+            keys = set(allowed)
+            keys.update(range(lo_blk * B, p + 1))
+            for t in keys:
+                if t <= p:
+                    vis[p, t] = True
+                else:
+                    raise AssertionError("a key after its query would be visible")
+    return vis
+
+
+def masked_attention(q, K, V, vis, scale=None):
+    """Dense softmax attention under an explicit mask, every head. fp64 [N, Hq, d]."""
+    N, Hq, d = q.shape
+    Hkv = K.shape[1]
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    out = np.empty_like(q)
+    for h in range(Hq):
+        g = h // G
+        s = (q[:, h, :] @ K[:N, g, :].T) * scale
+        s = np.where(vis, s, -np.inf)
+        s = s - s.max(axis=1, keepdims=True)
+        w = np.exp(s)
+        out[:, h, :] = (w @ V[:N, g, :]) / w.sum(axis=1, keepdims=True)
+    return out
+
+
+def brute_prefill(q_bits, k_pages, v_pages, block_table, n_tokens, L, B, S, W, k, cluster_start,
+                  score_scale=1.0):
+    q = widen(q_bits)
+    K = unpage(k_pages, block_table)
+    V = unpage(v_pages, block_table)
+    Hkv = k_pages.shape[1]
+    layout = cluster_layout(n_tokens, L, B, S, W, cluster_start)
+    sels, scores = [], []
+    for (s, e, a_end, lo_blk, sink_eff, cand) in layout:
+        sc = brute_scores(q, K, range(s, a_end), cand, B, Hkv, score_scale)
+        scores.append(sc)
+        sels.append(brute_select(sc, k))
+    vis = visibility_mask(n_tokens, layout, sels, B)
+    return {"layout": layout, "scores": scores, "selections": sels, "mask": vis,
+            "output": masked_attention(q, K, V, vis)}
