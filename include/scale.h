@@ -1,0 +1,176 @@
+/*
+ * scale.h -- C ABI of the MI355X (gfx950) cluster-level sparse-prefill library (libscale.so).
+ *
+ * The method is Similarity Chunk Rolling (SCR): during chunked prefill, the query sub-chunks of
+ * an outer chunk are grouped into clusters of consecutive sub-chunks, the KV-selection function
+ * runs once per cluster with the cluster's anchor fingerprint, and every member attends to the
+ * shared selection plus attention sinks and a cluster-spanning local window (paper Sec. 5.1,
+ * Eqs. 9 and 10, Algorithm 2). This library implements its per-layer hot path in block form:
+ *
+ *   scale_rep_keys        one representative key per KV block (mean of the block's keys)
+ *   scale_select_cluster  anchor fingerprint, head soft-voting over candidate blocks, top-k,
+ *                         once per cluster
+ *   scale_sparse_prefill  block-sparse attention of every query row over sink blocks, the
+ *                         cluster's selected blocks and the causal local window
+ *
+ * Conventions shared by every call:
+ *  - Plain C; no HIP or framework types. bf16 tensors are passed as uint16_t bit patterns.
+ *  - Device pointers are caller-owned device allocations (any HIP allocation visible to the
+ *    handle's device). The only host pointer is `cluster_start`.
+ *  - Every call validates all arguments on the host BEFORE any device work and returns a status;
+ *    on error nothing is launched and no output is touched. Calls enqueue on the stream given to
+ *    scale_init and return without synchronising; a kernel fault surfaces at the caller's next
+ *    synchronisation. No C++ exception crosses this boundary.
+ *  - A handle is not thread-safe: use one handle per stream. Calls on one handle are ordered by
+ *    its stream; the handle's scratch is reused by the next call only after the previous call's
+ *    kernels, which the stream order guarantees.
+ *
+ * Layouts (row-major, innermost last; Hq query heads, Hkv KV heads, d = head_dim,
+ * B = block_size, N = n_tokens, nb = N / B):
+ *    q       bf16  [N][Hq][d]             token-major queries of the outer chunk
+ *    k_pages bf16  [n_pages][Hkv][B][d]   paged key cache, one page = one block of B tokens
+ *    v_pages bf16  [n_pages][Hkv][B][d]   paged value cache, same paging as k_pages
+ *    block_table int32 [nb]               page holding logical block b; NULL = identity
+ *    k_rep   fp32  [nb][Hkv][d]           representative keys
+ *    sel_idx int32 [n_clusters][top_k]    selected blocks per cluster, ascending, -1 padded
+ *    sel_cnt int32 [n_clusters]           number of valid entries of each sel_idx row
+ *    out     fp32 or bf16 [N][Hq][d]      attention output (config.out_dtype)
+ * Query head h reads KV head floor(h * Hkv / Hq) (consecutive query heads share a KV head).
+ *
+ * Cluster geometry (cluster j covers sub-chunks [cluster_start[j], cluster_start[j+1]); L is the
+ * sub-chunk size, S the sink tokens, W the base local window, k the top-k):
+ *    s = cluster_start[j] * L,  e = min(cluster_start[j+1] * L, N),  anchor rows [s, min(s+L, e))
+ *    lo_blk   = max(0, min(s, e - W)) / B         local window starts at token lo_blk * B
+ *    sink_blk = ceil(S / B),  sink_eff = min(sink_blk, lo_blk)   sink blocks [0, sink_eff)
+ *    candidates: blocks [sink_blk, lo_blk)  (n_cand = max(0, lo_blk - sink_blk))
+ *    sel_cnt  = min(k, n_cand)
+ *    keys of row p in [s, e): sink blocks U selected blocks U tokens [lo_blk * B, p]
+ * The three key groups are disjoint and every key lies at or before its query (causal).
+ */
+#ifndef SCALE_H_
+#define SCALE_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct scale_ctx* scale_handle;
+
+typedef enum {
+  SCALE_OK = 0,
+  SCALE_ERR_INVALID_ARG = -1,   /* null pointer, inconsistent sizes, malformed cluster_start */
+  SCALE_ERR_UNSUPPORTED = -2,   /* valid but outside what this build supports (head_dim, B, ...) */
+  SCALE_ERR_OUT_OF_MEMORY = -3, /* scratch allocation failed in scale_init */
+  SCALE_ERR_CAPACITY = -4,      /* n_tokens or n_clusters above the capacity given to scale_init */
+  SCALE_ERR_HIP = -5            /* a HIP runtime call failed (no device, launch failure, ...) */
+} scale_status;
+
+typedef enum { SCALE_OUT_F32 = 0, SCALE_OUT_BF16 = 1 } scale_out_dtype;
+
+typedef struct {
+  int32_t num_q_heads;   /* Hq >= 1, a multiple of num_kv_heads                              */
+  int32_t num_kv_heads;  /* Hkv >= 1                                                         */
+  int32_t head_dim;      /* d: 64 or 128                                                     */
+  int32_t block_size;    /* B: 64 or 128 tokens per KV block / page                          */
+  int32_t sub_chunk;     /* L: query rows per sub-chunk, a positive multiple of B            */
+  int32_t top_k;         /* k >= 0 blocks selected per cluster (at most 64)                  */
+  int32_t sink_tokens;   /* S >= 0: attention-sink tokens, rounded up to whole blocks        */
+  int32_t local_window;  /* W >= 0: base local window in tokens                              */
+  int32_t max_tokens;    /* capacity: largest n_tokens any call will pass (sizes scratch)    */
+  int32_t max_clusters;  /* capacity: largest n_clusters any call will pass                  */
+  float softmax_scale;   /* attention logit scale; 0 means 1/sqrt(head_dim) (Eqs. 1, 10)     */
+  float score_scale;     /* selection logit scale sigma; 0 means 1.0 (the literal v . k)     */
+  int32_t out_dtype;     /* scale_out_dtype of the attention output                          */
+} scale_config;
+
+/* Create a handle bound to the current HIP device and to `hip_stream` (a hipStream_t; NULL is
+ * the default stream). Validates `cfg` first (INVALID_ARG / UNSUPPORTED before any HIP call),
+ * then allocates the scratch the calls need for cfg->max_tokens and cfg->max_clusters, once.
+ * On success *out holds the handle; on failure *out is NULL. Paper: the per-layer inputs of
+ * Algorithm 2 (Q, the KV cache, L, the budgets k, n_init and n_local). */
+scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle* out);
+
+/* Release the handle and its scratch (synchronises the handle's stream first). NULL is a no-op. */
+void scale_free(scale_handle h);
+
+/* Representative keys: k_rep[b][g][:] = mean over the B tokens of block b of K[t][g][:], for
+ * every logical block b < n_tokens / B. Accumulation is exact for bf16 inputs of moderate
+ * exponent range (fp64 sums), rounded once to fp32. The paper selects token by token; selecting
+ * KV blocks scored by a representative key is this library's block-level form of the selection
+ * function of Eq. 4 / Eq. 9.
+ * Requires n_tokens % block_size == 0 and 0 < n_tokens <= max_tokens. */
+scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32_t* block_table,
+                            int32_t n_tokens, float* k_rep);
+
+/* Cluster-level selection (Eq. 9 with head soft-voting, Sec. 5.1.3), once per cluster:
+ *   v[h]     = mean of q[p][h] over the anchor rows                      (Eq. 6 on the anchor)
+ *   x[h][b]  = score_scale * v[h] . k_rep[b][g(h)]      for candidate blocks b
+ *   score[b] = sum over h of softmax over candidates of x[h][.]   evaluated at b
+ *   sel      = top sel_cnt candidates by (score descending, block index ascending), emitted in
+ *              ascending block order into sel_idx[j][0..sel_cnt), the rest of the row is -1.
+ * cluster_start: HOST int32[n_clusters + 1], cluster_start[0] = 0, strictly increasing,
+ *   cluster_start[n_clusters] = ceil(n_tokens / sub_chunk).
+ * sel_cnt (device) receives min(k, n_cand) per cluster (also host-computable from the geometry).
+ * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens / B]; candidate entries
+ *   receive their score, every other entry -1.
+ * fingerprints_out (optional, may be NULL): device fp32 [n_clusters][Hq][d] anchor fingerprints.
+ * Each call adds n_clusters to the handle's retrieval-call counter. */
+scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens,
+                                  const float* k_rep, const int32_t* cluster_start,
+                                  int32_t n_clusters, int32_t* sel_idx, int32_t* sel_cnt,
+                                  float* scores_out, float* fingerprints_out);
+
+/* Block-sparse prefill attention (Eq. 10): for every row p of every cluster and every query
+ * head h, out[p][h] = softmax over Kset(p) of (q[p][h] . k_t * softmax_scale) weighted sum of
+ * v_t, with Kset(p) = sink blocks U sel_idx[j][0..sel_cnt[j]) U tokens [lo_blk * B, p].
+ * sel_idx / sel_cnt are device arrays as written by scale_select_cluster (any ascending or
+ * unordered set of distinct candidate blocks is accepted; entries are not re-validated on the
+ * device beyond clamping sel_cnt to [0, top_k]). cluster_start is the same host array as for
+ * the selection. bf16 output is the round-to-nearest-even of the fp32 result. */
+scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint16_t* k_pages,
+                                  const uint16_t* v_pages, const int32_t* block_table,
+                                  int32_t n_tokens, const int32_t* cluster_start,
+                                  int32_t n_clusters, const int32_t* sel_idx,
+                                  const int32_t* sel_cnt, void* out);
+
+/* Static text for a status code. Never NULL. */
+const char* scale_status_string(scale_status s);
+
+/* Cumulative number of selection calls (clusters) issued on this handle (Sec. 5.1.2). */
+scale_status scale_retrieval_calls(scale_handle h, int64_t* calls);
+
+/* Stages of the path, for scale_stage_times. */
+typedef enum {
+  SCALE_STAGE_REP_KEYS = 0,     /* representative-key reduction                          */
+  SCALE_STAGE_FINGERPRINT = 1,  /* anchor fingerprints (two kernels)                     */
+  SCALE_STAGE_LOGITS = 2,       /* per-head block logits                                 */
+  SCALE_STAGE_VOTE_TOPK = 3,    /* soft-voting scores and top-k                          */
+  SCALE_STAGE_ATTENTION = 4,    /* block-sparse attention                                */
+  SCALE_NUM_STAGES = 5
+} scale_stage;
+
+/* Device-time instrumentation (off by default). While enabled, every stage's kernels of every
+ * call are bracketed by a pair of HIP events on the handle's stream (event objects are created
+ * on first use and recycled). */
+scale_status scale_enable_timing(scale_handle h, int enable);
+
+/* Synchronises the handle's stream, then writes the accumulated device milliseconds and the
+ * number of timed launches of each stage (arrays of SCALE_NUM_STAGES) since the last reset.
+ * Either output may be NULL. reset != 0 zeroes the accumulators afterwards. */
+scale_status scale_stage_times(scale_handle h, double* ms, int64_t* launches, int reset);
+
+/* Host-only geometry of each cluster, exactly as the calls above use it (no HIP call; usable
+ * without a device). For cluster j, writes geo[j*6 + 0..5] =
+ *   { s, e, lo_blk, sink_eff, n_cand, sel_cnt }.
+ * Same validation of cfg and cluster_start as the calls above. */
+scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens,
+                                    const int32_t* cluster_start, int32_t n_clusters,
+                                    int32_t* geo);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCALE_H_ */

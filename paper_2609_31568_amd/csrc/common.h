@@ -1,0 +1,70 @@
+// Internal declarations shared by the host runtime and the gfx950 kernels of libscale.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace scale {
+
+// Geometry of one cluster as the kernels read it (see include/scale.h for the definitions).
+struct ClusterGeo {
+  int32_t s;         // first query row
+  int32_t e;         // one past the last query row
+  int32_t anchor_end;
+  int32_t lo_blk;    // local window starts at token lo_blk * B
+  int32_t sink_eff;  // sink blocks [0, sink_eff)
+  int32_t n_cand;    // candidate blocks [sink_blk, sink_blk + n_cand)
+  int32_t sel_cnt;   // min(top_k, n_cand)
+  int32_t pad;
+};
+static_assert(sizeof(ClusterGeo) == 32, "ClusterGeo is uploaded as raw bytes");
+
+// One attention work item: a tile of query positions of one cluster for one KV head group.
+struct WorkItem {
+  int32_t cluster;
+  int32_t kv_head;
+  int32_t p0;        // first query position of the tile
+  int32_t n_rows;    // positions in the tile (<= the tile size)
+};
+static_assert(sizeof(WorkItem) == 16, "WorkItem is uploaded as raw bytes");
+
+// ---- launchers (each defined next to its kernel) ----
+
+// k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32).
+hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int n_blocks,
+                           int num_kv_heads, int block_size, int head_dim, float* k_rep,
+                           hipStream_t stream);
+
+// Anchor fingerprints: partial fp64 row sums per (cluster, row chunk), then fp32 means.
+// `partial` holds n_clusters * fp_chunks * Hq * d doubles.
+hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
+                               int num_q_heads, int head_dim, int sub_chunk, int fp_chunks,
+                               double* partial, float* fingerprints, hipStream_t stream);
+
+// Selection logits x[j][h][c] for candidate c of cluster j (row stride `cand_stride`).
+hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
+                               int n_clusters, int max_cand, int cand_stride, int sink_blk,
+                               int num_q_heads, int num_kv_heads, int head_dim, float score_scale,
+                               float* logits, hipStream_t stream);
+
+// Soft-voting scores and deterministic top-k per cluster.
+hipError_t launch_vote_topk(const float* logits, const ClusterGeo* geo, int n_clusters,
+                            int cand_stride, int sink_blk, int num_q_heads, int top_k,
+                            int n_blocks, float* scores_lds_spill, int32_t* sel_idx,
+                            int32_t* sel_cnt, float* scores_out, hipStream_t stream);
+
+// Block-sparse attention over the work list.
+hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
+                                   const int32_t* block_table, const ClusterGeo* geo,
+                                   const WorkItem* items, int n_items, const int32_t* sel_idx,
+                                   const int32_t* sel_cnt, int top_k, int num_q_heads,
+                                   int num_kv_heads, int head_dim, int block_size, int n_blocks,
+                                   float qk_scale_log2, int out_bf16, void* out, hipStream_t stream);
+
+// Row chunks of fingerprint_partial for a sub-chunk of `sub_chunk` rows.
+int fingerprint_chunks(int sub_chunk);
+
+// Positions per attention work item (query rows per KV head group of one work-group).
+constexpr int kTilePositions = 32;
+
+}  // namespace scale

@@ -1,0 +1,421 @@
+// Host runtime of libscale: argument validation, cluster geometry, scratch, the attention work
+// list, and the launches behind the C ABI declared in include/scale.h.
+//
+// Every entry point validates on the host before touching the device. Per-call metadata (the
+// cluster geometry and the attention work list) is written into a ring of pinned host slots and
+// copied to device scratch asynchronously on the handle's stream; a slot is reused only after
+// the event recorded behind its copy has completed.
+#include "../../include/scale.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.h"
+
+namespace {
+
+using scale::ClusterGeo;
+using scale::WorkItem;
+
+constexpr int kRingSlots = 4;
+
+struct Slot {
+  void* host = nullptr;      // pinned
+  hipEvent_t done = nullptr; // recorded after the copy that reads `host`
+  bool pending = false;
+};
+
+struct TimedLaunch {
+  int stage;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct scale_ctx {
+  scale_config cfg{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int64_t retrieval_calls = 0;
+  int max_blocks = 0;        // max_tokens / B (rounded up)
+  int fp_chunks = 0;
+  int max_items = 0;
+  // device scratch
+  ClusterGeo* d_geo = nullptr;
+  WorkItem* d_items = nullptr;
+  double* d_fp_partial = nullptr;
+  float* d_fingerprints = nullptr;
+  float* d_logits = nullptr;
+  float* d_spill = nullptr;
+  // pinned staging ring
+  size_t slot_bytes = 0;
+  Slot slots[kRingSlots];
+  int next_slot = 0;
+  // stage timing
+  bool timing = false;
+  std::vector<TimedLaunch> timed;       // recorded, not yet read
+  std::vector<hipEvent_t> spare_events; // recycled
+  double stage_ms[SCALE_NUM_STAGES] = {};
+  int64_t stage_launches[SCALE_NUM_STAGES] = {};
+  hipEvent_t open_start = nullptr;
+};
+
+namespace {
+
+scale_status validate_config(const scale_config* c) {
+  if (!c) return SCALE_ERR_INVALID_ARG;
+  if (c->num_q_heads < 1 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads) return SCALE_ERR_INVALID_ARG;
+  if (c->head_dim < 1 || c->block_size < 1 || c->sub_chunk < 1) return SCALE_ERR_INVALID_ARG;
+  if (c->top_k < 0 || c->sink_tokens < 0 || c->local_window < 0) return SCALE_ERR_INVALID_ARG;
+  if (c->max_tokens < 1 || c->max_clusters < 1) return SCALE_ERR_INVALID_ARG;
+  if (!std::isfinite(c->softmax_scale) || c->softmax_scale < 0.f) return SCALE_ERR_INVALID_ARG;
+  if (!std::isfinite(c->score_scale)) return SCALE_ERR_INVALID_ARG;
+  if (c->out_dtype != SCALE_OUT_F32 && c->out_dtype != SCALE_OUT_BF16) return SCALE_ERR_INVALID_ARG;
+  if (c->head_dim != 64 && c->head_dim != 128) return SCALE_ERR_UNSUPPORTED;
+  if (c->block_size != 64 && c->block_size != 128) return SCALE_ERR_UNSUPPORTED;
+  if (c->sub_chunk % c->block_size) return SCALE_ERR_UNSUPPORTED;
+  if (c->num_q_heads / c->num_kv_heads > 8) return SCALE_ERR_UNSUPPORTED;
+  // sizes that keep every int32 index of the kernels in range
+  if ((int64_t)c->max_tokens * c->num_q_heads * c->head_dim >= ((int64_t)1 << 40)) return SCALE_ERR_UNSUPPORTED;
+  return SCALE_OK;
+}
+
+// Validates n_tokens and cluster_start against the config; fills the geometry when geo != null.
+scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_t* cluster_start,
+                           int32_t n_clusters, ClusterGeo* geo) {
+  if (!cluster_start || n_clusters < 1 || n_tokens < 1) return SCALE_ERR_INVALID_ARG;
+  if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
+  if (n_tokens > c.max_tokens || n_clusters > c.max_clusters) return SCALE_ERR_CAPACITY;
+  const int64_t M = ((int64_t)n_tokens + c.sub_chunk - 1) / c.sub_chunk;
+  if (cluster_start[0] != 0 || cluster_start[n_clusters] != M) return SCALE_ERR_INVALID_ARG;
+  for (int j = 0; j < n_clusters; ++j)
+    if (cluster_start[j + 1] <= cluster_start[j]) return SCALE_ERR_INVALID_ARG;
+  if (!geo) return SCALE_OK;
+  const int B = c.block_size;
+  const int sink_blk = (c.sink_tokens + B - 1) / B;
+  for (int j = 0; j < n_clusters; ++j) {
+    ClusterGeo& g = geo[j];
+    g.s = (int32_t)((int64_t)cluster_start[j] * c.sub_chunk);
+    g.e = (int32_t)std::min<int64_t>((int64_t)cluster_start[j + 1] * c.sub_chunk, n_tokens);
+    g.anchor_end = std::min(g.s + c.sub_chunk, g.e);
+    const int lo = std::max(0, std::min(g.s, g.e - c.local_window));
+    g.lo_blk = lo / B;
+    g.sink_eff = std::min(sink_blk, g.lo_blk);
+    g.n_cand = std::max(0, g.lo_blk - sink_blk);
+    g.sel_cnt = std::min(c.top_k, g.n_cand);
+    g.pad = 0;
+  }
+  return SCALE_OK;
+}
+
+int64_t max_work_items(const scale_config& c) {
+  const int64_t tiles = ((int64_t)c.max_tokens + scale::kTilePositions - 1) / scale::kTilePositions + c.max_clusters;
+  return tiles * c.num_kv_heads;
+}
+
+hipEvent_t take_event(scale_ctx* h) {
+  if (!h->spare_events.empty()) {
+    hipEvent_t e = h->spare_events.back();
+    h->spare_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Opens / closes the timing bracket of one stage (no-ops unless timing is enabled).
+void stage_begin(scale_ctx* h) {
+  if (!h->timing) return;
+  h->open_start = take_event(h);
+  if (h->open_start) (void)hipEventRecord(h->open_start, h->stream);
+}
+void stage_end(scale_ctx* h, int stage) {
+  if (!h->timing || !h->open_start) return;
+  hipEvent_t stop = take_event(h);
+  if (stop && hipEventRecord(stop, h->stream) == hipSuccess) {
+    h->timed.push_back({stage, h->open_start, stop});
+  } else {
+    h->spare_events.push_back(h->open_start);
+    if (stop) h->spare_events.push_back(stop);
+  }
+  h->open_start = nullptr;
+}
+
+void release(scale_ctx* h) {
+  if (!h) return;
+  for (auto& t : h->timed) {
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  for (auto e : h->spare_events) (void)hipEventDestroy(e);
+  for (auto& s : h->slots) {
+    if (s.done) (void)hipEventDestroy(s.done);
+    if (s.host) (void)hipHostFree(s.host);
+  }
+  (void)hipFree(h->d_geo);
+  (void)hipFree(h->d_items);
+  (void)hipFree(h->d_fp_partial);
+  (void)hipFree(h->d_fingerprints);
+  (void)hipFree(h->d_logits);
+  (void)hipFree(h->d_spill);
+  delete h;
+}
+
+// Next pinned staging slot, waiting (rarely) for the copy that last read it.
+scale_status acquire_slot(scale_ctx* h, Slot** out) {
+  Slot& s = h->slots[h->next_slot];
+  h->next_slot = (h->next_slot + 1) % kRingSlots;
+  if (s.pending) {
+    if (hipEventSynchronize(s.done) != hipSuccess) return SCALE_ERR_HIP;
+    s.pending = false;
+  }
+  *out = &s;
+  return SCALE_OK;
+}
+
+// Copies the first `bytes` of the slot to `dst` and marks the slot busy until the copy is done.
+scale_status upload(scale_ctx* h, Slot* s, void* dst, size_t bytes) {
+  if (bytes == 0) return SCALE_OK;
+  if (hipMemcpyAsync(dst, s->host, bytes, hipMemcpyHostToDevice, h->stream) != hipSuccess) return SCALE_ERR_HIP;
+  if (hipEventRecord(s->done, h->stream) != hipSuccess) return SCALE_ERR_HIP;
+  s->pending = true;
+  return SCALE_OK;
+}
+
+scale_status check_launch(hipError_t e) { return e == hipSuccess ? SCALE_OK : SCALE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* scale_status_string(scale_status s) {
+  switch (s) {
+    case SCALE_OK: return "ok";
+    case SCALE_ERR_INVALID_ARG: return "invalid argument";
+    case SCALE_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SCALE_ERR_OUT_OF_MEMORY: return "out of device or pinned memory";
+    case SCALE_ERR_CAPACITY: return "size above the capacity given to scale_init";
+    case SCALE_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens, const int32_t* cluster_start,
+                                    int32_t n_clusters, int32_t* geo_out) {
+  scale_status st = validate_config(cfg);
+  if (st != SCALE_OK) return st;
+  if (!geo_out) return SCALE_ERR_INVALID_ARG;
+  st = plan_geometry(*cfg, n_tokens, cluster_start, n_clusters, nullptr);
+  if (st != SCALE_OK) return st;
+  std::vector<ClusterGeo> geo(n_clusters);
+  plan_geometry(*cfg, n_tokens, cluster_start, n_clusters, geo.data());
+  for (int j = 0; j < n_clusters; ++j) {
+    const ClusterGeo& g = geo[j];
+    int32_t* o = geo_out + 6 * j;
+    o[0] = g.s; o[1] = g.e; o[2] = g.lo_blk; o[3] = g.sink_eff; o[4] = g.n_cand; o[5] = g.sel_cnt;
+  }
+  return SCALE_OK;
+}
+
+scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle* out) {
+  if (!out) return SCALE_ERR_INVALID_ARG;
+  *out = nullptr;
+  scale_status st = validate_config(cfg);
+  if (st != SCALE_OK) return st;
+
+  scale_ctx* h = new (std::nothrow) scale_ctx();
+  if (!h) return SCALE_ERR_OUT_OF_MEMORY;
+  h->cfg = *cfg;
+  h->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  if (hipGetDevice(&h->device) != hipSuccess) { release(h); return SCALE_ERR_HIP; }
+  const scale_config& c = h->cfg;
+  h->max_blocks = (c.max_tokens + c.block_size - 1) / c.block_size;
+  h->fp_chunks = scale::fingerprint_chunks(c.sub_chunk);
+  h->max_items = (int)max_work_items(c);
+  const int64_t row_elems = (int64_t)c.num_q_heads * c.head_dim;
+  const int64_t mc = c.max_clusters;
+
+  auto dev = [&](void** p, size_t bytes) -> bool {
+    if (bytes == 0) return true;
+    return hipMalloc(p, bytes) == hipSuccess;
+  };
+  bool ok = dev((void**)&h->d_geo, sizeof(ClusterGeo) * mc) &&
+            dev((void**)&h->d_items, sizeof(WorkItem) * (size_t)h->max_items) &&
+            dev((void**)&h->d_fp_partial, sizeof(double) * mc * h->fp_chunks * row_elems) &&
+            dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
+            dev((void**)&h->d_logits, sizeof(float) * mc * c.num_q_heads * (int64_t)h->max_blocks) &&
+            dev((void**)&h->d_spill, h->max_blocks > 8192 ? sizeof(float) * mc * h->max_blocks : 0);
+  if (!ok) {
+    (void)hipGetLastError();
+    release(h);
+    return SCALE_ERR_OUT_OF_MEMORY;
+  }
+  h->slot_bytes = std::max(sizeof(ClusterGeo) * mc + sizeof(WorkItem) * (size_t)h->max_items, (size_t)256);
+  for (auto& s : h->slots) {
+    if (hipHostMalloc(&s.host, h->slot_bytes, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      release(h);
+      return SCALE_ERR_OUT_OF_MEMORY;
+    }
+  }
+  *out = h;
+  return SCALE_OK;
+}
+
+void scale_free(scale_handle h) {
+  if (!h) return;
+  (void)hipStreamSynchronize(h->stream);
+  release(h);
+}
+
+scale_status scale_retrieval_calls(scale_handle h, int64_t* calls) {
+  if (!h || !calls) return SCALE_ERR_INVALID_ARG;
+  *calls = h->retrieval_calls;
+  return SCALE_OK;
+}
+
+scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32_t* block_table, int32_t n_tokens,
+                            float* k_rep) {
+  if (!h || !k_pages || !k_rep || n_tokens < 1) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
+  if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
+  stage_begin(h);
+  const hipError_t e = scale::launch_rep_keys(k_pages, block_table, n_tokens / c.block_size, c.num_kv_heads,
+                                              c.block_size, c.head_dim, k_rep, h->stream);
+  stage_end(h, SCALE_STAGE_REP_KEYS);
+  return check_launch(e);
+}
+
+scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens, const float* k_rep,
+                                  const int32_t* cluster_start, int32_t n_clusters, int32_t* sel_idx,
+                                  int32_t* sel_cnt, float* scores_out, float* fingerprints_out) {
+  if (!h || !q || !k_rep || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  if (st != SCALE_OK) return st;
+
+  Slot* slot = nullptr;
+  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
+  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  int max_cand = 0;
+  for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
+  if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
+
+  const int n_blocks = n_tokens / c.block_size;
+  const int sink_blk = (c.sink_tokens + c.block_size - 1) / c.block_size;
+  const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
+  float* fps = fingerprints_out ? fingerprints_out : h->d_fingerprints;
+  stage_begin(h);
+  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, c.sub_chunk,
+                                               h->fp_chunks, h->d_fp_partial, fps, h->stream));
+  stage_end(h, SCALE_STAGE_FINGERPRINT);
+  if (st != SCALE_OK) return st;
+  stage_begin(h);
+  st = check_launch(scale::launch_block_logits(fps, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
+                                               c.num_q_heads, c.num_kv_heads, c.head_dim, sigma, h->d_logits,
+                                               h->stream));
+  stage_end(h, SCALE_STAGE_LOGITS);
+  if (st != SCALE_OK) return st;
+  stage_begin(h);
+  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_geo, n_clusters, h->max_blocks, sink_blk,
+                                            c.num_q_heads, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
+                                            scores_out, h->stream));
+  stage_end(h, SCALE_STAGE_VOTE_TOPK);
+  if (st != SCALE_OK) return st;
+  h->retrieval_calls += n_clusters;
+  return SCALE_OK;
+}
+
+scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
+                                  const int32_t* block_table, int32_t n_tokens, const int32_t* cluster_start,
+                                  int32_t n_clusters, const int32_t* sel_idx, const int32_t* sel_cnt, void* out) {
+  if (!h || !q || !k_pages || !v_pages || !sel_idx || !sel_cnt || !out) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  if (st != SCALE_OK) return st;
+
+  Slot* slot = nullptr;
+  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
+  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  WorkItem* items = reinterpret_cast<WorkItem*>(geo + n_clusters);
+
+  // Work list: (cluster, position tile) ordered by decreasing key count, each for every KV head.
+  const int B = c.block_size;
+  const int TP = scale::kTilePositions;
+  struct Tile { int64_t cost; int32_t cluster, p0, n_rows; };
+  std::vector<Tile> tiles;
+  tiles.reserve((size_t)(n_tokens / TP + n_clusters));
+  for (int j = 0; j < n_clusters; ++j) {
+    const ClusterGeo& g = geo[j];
+    for (int p0 = g.s; p0 < g.e; p0 += TP) {
+      const int nr = std::min(TP, g.e - p0);
+      const int64_t keys = (int64_t)(g.sink_eff + g.sel_cnt) * B + (p0 + nr - g.lo_blk * B);
+      tiles.push_back({keys, j, p0, nr});
+    }
+  }
+  std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& a, const Tile& b) { return a.cost > b.cost; });
+  const int64_t n_items = (int64_t)tiles.size() * c.num_kv_heads;
+  if (n_items > h->max_items) return SCALE_ERR_CAPACITY;
+  int64_t k = 0;
+  for (const Tile& t : tiles)
+    for (int g = 0; g < c.num_kv_heads; ++g) items[k++] = {t.cluster, g, t.p0, t.n_rows};
+
+  // geometry and items sit back to back in the slot; they go to two device buffers
+  if (hipMemcpyAsync(h->d_geo, geo, sizeof(ClusterGeo) * n_clusters, hipMemcpyHostToDevice, h->stream) != hipSuccess ||
+      hipMemcpyAsync(h->d_items, items, sizeof(WorkItem) * (size_t)n_items, hipMemcpyHostToDevice, h->stream) !=
+          hipSuccess ||
+      hipEventRecord(slot->done, h->stream) != hipSuccess)
+    return SCALE_ERR_HIP;
+  slot->pending = true;
+
+  const float scale = c.softmax_scale == 0.f ? 1.0f / std::sqrt((float)c.head_dim) : c.softmax_scale;
+  const float qk_scale_log2 = scale * 1.4426950408889634f;
+  stage_begin(h);
+  const hipError_t e = scale::launch_sparse_attention(q, k_pages, v_pages, block_table, h->d_geo, h->d_items,
+                                                      (int)n_items, sel_idx, sel_cnt, c.top_k, c.num_q_heads,
+                                                      c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
+                                                      c.out_dtype == SCALE_OUT_BF16, out, h->stream);
+  stage_end(h, SCALE_STAGE_ATTENTION);
+  return check_launch(e);
+}
+
+scale_status scale_enable_timing(scale_handle h, int enable) {
+  if (!h) return SCALE_ERR_INVALID_ARG;
+  h->timing = enable != 0;
+  return SCALE_OK;
+}
+
+scale_status scale_stage_times(scale_handle h, double* ms, int64_t* launches, int reset) {
+  if (!h) return SCALE_ERR_INVALID_ARG;
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return SCALE_ERR_HIP;
+  for (const TimedLaunch& t : h->timed) {
+    float e = 0.f;
+    if (hipEventElapsedTime(&e, t.start, t.stop) != hipSuccess) return SCALE_ERR_HIP;
+    h->stage_ms[t.stage] += e;
+    h->stage_launches[t.stage] += 1;
+    h->spare_events.push_back(t.start);
+    h->spare_events.push_back(t.stop);
+  }
+  h->timed.clear();
+  for (int i = 0; i < SCALE_NUM_STAGES; ++i) {
+    if (ms) ms[i] = h->stage_ms[i];
+    if (launches) launches[i] = h->stage_launches[i];
+    if (reset) {
+      h->stage_ms[i] = 0.0;
+      h->stage_launches[i] = 0;
+    }
+  }
+  return SCALE_OK;
+}
+
+}  // extern "C"

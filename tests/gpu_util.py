@@ -1,0 +1,184 @@
+"""Helpers for the GPU parity tests: upload generator inputs, run the library through its C ABI,
+and compare with the oracle under the acceptance rules."""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import gen
+import oracle
+
+# Acceptance on the attention output (max-abs and relative L2 against the fp64 oracle).
+O_MAX_ABS = 1e-2
+O_REL_L2 = 5e-3
+# Selected indices must equal the oracle's wherever the top-k margin exceeds this.
+MARGIN = 1e-3
+
+
+def log(msg: str):
+    print(msg, flush=True)
+
+
+def to_dev(a: np.ndarray, dev):
+    import torch
+
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(dev)
+    return torch.from_numpy(a).to(dev)
+
+
+def config(w: gen.Workload, n_clusters: int, out_bf16=False, **over):
+    import paper_2609_31568_amd as pk
+
+    kw = dict(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
+              block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=w.top_k, sink_tokens=w.sink_tokens,
+              local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=n_clusters)
+    kw.update(over)
+    return pk.config_for(out_bf16=out_bf16, **kw)
+
+
+def run_gpu(w: gen.Workload, data: dict, cs, dev, *, out_bf16=False, n_tokens=None, with_scores=True, **over):
+    """Whole path on the GPU; returns host copies of every output plus the call counter."""
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    n = w.n_tokens if n_tokens is None else n_tokens
+    cfg = config(w, len(cs) - 1, out_bf16=out_bf16, **over)
+    q = to_dev(data["q"][:n], dev)
+    kp = to_dev(data["k_pages"], dev)
+    vp = to_dev(data["v_pages"], dev)
+    bt = to_dev(data["block_table"], dev)
+    with pk.Scale(cfg) as h:
+        bufs = pk.LayerBuffers(cfg, n, len(cs) - 1, device=dev, with_scores=with_scores)
+        pk.run_layer(h, q, kp, vp, bt, n, cs, bufs)
+        torch.cuda.synchronize()
+        calls = h.retrieval_calls()
+    res = {
+        "k_rep": bufs.k_rep.cpu().numpy(),
+        "sel_idx": bufs.sel_idx.cpu().numpy(),
+        "sel_cnt": bufs.sel_cnt.cpu().numpy(),
+        "out": bufs.out.float().cpu().numpy() if not out_bf16 else bufs.out.view(torch.int16).cpu().numpy(),
+        "calls": calls,
+    }
+    if with_scores:
+        res["scores"] = bufs.scores.cpu().numpy()
+        res["fingerprints"] = bufs.fingerprints.cpu().numpy()
+    return res
+
+
+def check_rounding(gpu: np.ndarray, ref: np.ndarray, what: str):
+    """GPU value = fp32 rounding of the fp64 result: |gpu - ref| <= 2^-24 |ref| (+ tiny)."""
+    err = np.abs(gpu.astype(np.float64) - ref)
+    bound = np.abs(ref) * 2.0 ** -24 + 1e-38
+    bad = err > bound
+    assert not bad.any(), f"{what}: {bad.sum()} values off by more than half an fp32 ulp, max {err.max():.3e}"
+
+
+U32 = 2.0 ** -24
+
+
+def score_bounds(ref, num_kv_heads: int, score_scale: float = 1.0):
+    """First-order error bound of the GPU's fp32 soft-voting scores, per cluster and candidate.
+
+    GPU logits are fp32 dot products of the fp32-rounded fingerprint and representative key:
+    |dx| <= (d + 2) u sum_i |v_i k_i| =: dX (recursive-summation bound plus the two input
+    roundings). A softmax weight p moves by at most 2 p dX under logit perturbations of at most
+    dX; the exponent's argument x - max carries a rounding of u |x - max|; exp, the normaliser
+    (n_cand terms) and the sum over heads add (n_cand + Hq + 8) u relative. Hence
+    |d score_b| <= score_b (2 dX + 2 u R + (n_cand + Hq + 8) u) + 1e-9, with R the logit range.
+    """
+    out = []
+    for g, v, sc in zip(ref["geometry"], ref["fingerprints"], ref["scores"]):
+        if g.n_cand == 0:
+            out.append(np.zeros(0))
+            continue
+        kr = ref["k_rep"][g.sink_blk:g.sink_blk + g.n_cand]        # [n, Hkv, d]
+        Hq, d = v.shape
+        heads_g = (np.arange(Hq) * num_kv_heads) // Hq
+        absdot = np.einsum("hi,nhi->hn", np.abs(v), np.abs(kr[:, heads_g, :])) * abs(score_scale)
+        dX = (d + 2) * U32 * absdot.max()
+        x = np.einsum("hi,nhi->hn", v, kr[:, heads_g, :]) * score_scale
+        R = float((x.max(axis=1) - x.min(axis=1)).max())
+        rel = 2 * dX + 2 * U32 * R + (g.n_cand + Hq + 8) * U32
+        out.append(sc * rel + 1e-9)
+    return out
+
+
+def check_scores(gpu_scores: np.ndarray, ref, num_kv_heads: int, what: str):
+    """Candidates within the bound above; every other entry of the row is -1."""
+    worst = 0.0
+    nb = gpu_scores.shape[1]
+    for j, (g, sc, bound) in enumerate(zip(ref["geometry"], ref["scores"], score_bounds(ref, num_kv_heads))):
+        row = gpu_scores[j]
+        cand = np.arange(g.sink_blk, g.sink_blk + g.n_cand)
+        assert np.all(np.delete(row, cand) == -1.0), f"{what} cluster {j}: non-candidate entry is not -1"
+        if g.n_cand:
+            err = np.abs(row[cand].astype(np.float64) - sc)
+            assert np.all(err <= bound), f"{what} cluster {j}: score error {err.max():.2e} above bound"
+            worst = max(worst, float(err.max()))
+        assert nb >= g.sink_blk + g.n_cand
+    return worst
+
+
+def check_selection(gpu_sel, gpu_cnt, ref, eps: float):
+    """Exact where the oracle's margin exceeds MARGIN; eps-valid top-k everywhere."""
+    n_exact = 0
+    for j, (g, s_ref, m, sc) in enumerate(zip(ref["geometry"], ref["selections"], ref["margins"], ref["scores"])):
+        cnt = int(gpu_cnt[j])
+        assert cnt == g.sel_cnt, f"cluster {j}: sel_cnt {cnt} != {g.sel_cnt}"
+        got = gpu_sel[j, :cnt].astype(np.int64)
+        assert np.all(gpu_sel[j, cnt:] == -1), f"cluster {j}: padding is not -1"
+        assert np.all(np.diff(got) > 0), f"cluster {j}: not strictly ascending"
+        assert np.all((got >= g.sink_blk) & (got < g.sink_blk + g.n_cand)), f"cluster {j}: non-candidate selected"
+        if m > MARGIN:
+            assert np.array_equal(got, s_ref), f"cluster {j}: {got} != oracle {s_ref} (margin {m:.2e})"
+            n_exact += 1
+        if 0 < cnt < g.n_cand:
+            kth = np.sort(sc)[::-1][cnt - 1]
+            chosen = np.zeros(g.n_cand, dtype=bool)
+            chosen[got - g.sink_blk] = True
+            assert np.all(sc[chosen] >= kth - eps), f"cluster {j}: a selected block is not within eps of top-k"
+            assert np.all(sc[~chosen] <= kth + eps), f"cluster {j}: an unselected block beats the k-th by > eps"
+    return n_exact
+
+
+def check_output(out: np.ndarray, ref: np.ndarray, what: str):
+    err = np.abs(out.astype(np.float64) - ref)
+    mx = float(err.max()) if err.size else 0.0
+    rel = float(np.linalg.norm(out.astype(np.float64) - ref) / max(np.linalg.norm(ref), 1e-300))
+    assert mx <= O_MAX_ABS and rel <= O_REL_L2, f"{what}: max-abs {mx:.3e}, rel-L2 {rel:.3e}"
+    return mx, rel
+
+
+def gpu_selections(res, n_clusters):
+    return [res["sel_idx"][j, :res["sel_cnt"][j]].astype(np.int64) for j in range(n_clusters)]
+
+
+def sample_rows(geo, rng, tiles_per_cluster=3, tile=32):
+    """A few 32-row tiles per cluster: its first and last tile plus random ones."""
+    out = []
+    for g in geo:
+        starts = {g.s, max(g.s, g.e - tile)}
+        n_t = max(1, (g.e - g.s) // tile)
+        for _ in range(tiles_per_cluster):
+            starts.add(g.s + int(rng.integers(0, n_t)) * tile)
+        rows = sorted({r for s0 in starts for r in range(s0, min(s0 + tile, g.e))})
+        out.append(np.asarray(rows, dtype=np.int64))
+    return out
+
+
+def bf16_rne(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits, round to nearest even (test-side reference of the epilogue)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    return r
+
+
+def nan_free(*arrays):
+    return all(not np.isnan(a).any() for a in arrays)
+
+
+def isfinite_margin(m):
+    return m if math.isfinite(m) else float("inf")

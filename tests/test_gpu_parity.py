@@ -1,0 +1,209 @@
+"""GPU parity: the HIP path, called through the C ABI, against the fp64 oracle on the same seeded
+inputs. Small shapes are compared element by element; the full-size workloads on every
+selection and on sampled attention rows."""
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+# eps of the eps-valid top-k check: far above the score error bound of gpu_util.score_bounds
+# (about 1e-4 of a score in the worst case, 1e-6 observed) and far below typical score gaps.
+EPS_VALID = 1e-5
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_31568_amd  # noqa: F401  (fails loudly if the library is missing)
+
+    return torch.device("cuda:0")
+
+
+def _oracle(w, d, cs, n=None, with_output=True, external_sel=None):
+    n = w.n_tokens if n is None else n
+    return oracle.prefill(d["q"][:n], d["k_pages"], d["v_pages"], d["block_table"], n, sub_chunk=w.sub_chunk,
+                          block_size=w.block_size, top_k=w.top_k, sink_tokens=w.sink_tokens,
+                          local_window=w.local_window, cluster_start=cs, with_output=with_output,
+                          external_sel=external_sel)
+
+
+SHAPES = {
+    # name: (workload, cluster size)
+    "tiny_c4": (gen.WORKLOADS["tiny"], 4),
+    "tiny_c1": (gen.WORKLOADS["tiny"], 1),
+    # GQA 4:1, d 128, B 128, cluster 3 of M = 16 (ragged last cluster), cluster longer than W
+    "gqa128": (gen.Workload("gqa128", 1, 8, 2, 128, 8192, 128, 512, 3, 5, 128, 1024, 12, 1, 4, 31), 3),
+    # group of 7 query heads, d 128, B 64
+    "g7": (gen.Workload("g7", 1, 14, 2, 128, 4096, 64, 256, 4, 6, 64, 512, 8, 1, 3, 32), 4),
+    # MHA (group 1), d 64, B 128, no sink, window not a block multiple
+    "g1": (gen.Workload("g1", 1, 2, 2, 64, 4096, 128, 512, 2, 3, 0, 700, 6, 1, 3, 33), 2),
+    # group 8, sink rounded up to 3 blocks, short window
+    "g8": (gen.Workload("g8", 1, 8, 1, 64, 2048, 64, 128, 5, 4, 130, 100, 6, 1, 5, 34), 5),
+}
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_small_shapes_full_parity(dev, name):
+    w, c = SHAPES[name]
+    gu.log(f"[parity] {name}")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs)
+    gu.check_rounding(res["k_rep"], ref["k_rep"], "k_rep")
+    gu.check_rounding(res["fingerprints"], np.stack(ref["fingerprints"]), "fingerprints")
+    gu.check_scores(res["scores"], ref, w.num_kv_heads, name)
+    gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, EPS_VALID)
+    assert res["calls"] == len(cs) - 1
+    # attention under the GPU's own selection, every row and head
+    own = _oracle(w, d, cs, external_sel=gu.gpu_selections(res, len(cs) - 1))
+    mx, rel = gu.check_output(res["out"], own["output"], f"{name} output")
+    gu.log(f"[parity] {name}: max-abs {mx:.2e} rel-L2 {rel:.2e}")
+    # and under the oracle's selection on clusters where both agree
+    for j, g in enumerate(ref["geometry"]):
+        if np.array_equal(gu.gpu_selections(res, len(cs) - 1)[j], ref["selections"][j]):
+            gu.check_output(res["out"][g.s:g.e], ref["output"][g.s:g.e], f"{name} cluster {j}")
+
+
+def test_dense_reduction_on_gpu(dev):
+    """top_k >= every candidate count: the GPU output must be dense causal attention."""
+    w = SHAPES["gqa128"][0].with_(top_k=64)
+    gu.log("[parity] dense reduction")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 3)
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs)
+    assert all(g.sel_cnt == g.n_cand for g in ref["geometry"])
+    gu.check_output(res["out"], ref["output"], "dense")
+
+
+def test_short_last_subchunk(dev):
+    """n_tokens = 2368: nine sub-chunks of 256 and a last one of 64; clusters of 4."""
+    w = gen.WORKLOADS["tiny"].with_(n_tokens=2368)
+    gu.log("[parity] short last sub-chunk")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 4)
+    assert cs[-1] == 10
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs)
+    gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, EPS_VALID)
+    own = _oracle(w, d, cs, external_sel=gu.gpu_selections(res, len(cs) - 1))
+    gu.check_output(res["out"], own["output"], "short tail")
+
+
+def test_bf16_output_is_rne_of_fp32(dev):
+    w, c = SHAPES["gqa128"]
+    gu.log("[parity] bf16 epilogue")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    r32 = gu.run_gpu(w, d, cs, dev)
+    r16 = gu.run_gpu(w, d, cs, dev, out_bf16=True)
+    assert np.array_equal(r16["out"].view(np.uint16), gu.bf16_rne(r32["out"]))
+
+
+def test_deterministic_and_page_permutation(dev):
+    w, c = SHAPES["g7"]
+    gu.log("[parity] determinism + paging")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    a = gu.run_gpu(w, d, cs, dev)
+    b = gu.run_gpu(w, d, cs, dev)
+    for key in ("k_rep", "sel_idx", "sel_cnt", "out", "scores", "fingerprints"):
+        assert np.array_equal(a[key], b[key]), key
+    perm = np.random.default_rng(3).permutation(w.n_blocks)
+    kp = np.empty_like(d["k_pages"])
+    vp = np.empty_like(d["v_pages"])
+    kp[perm] = d["k_pages"]
+    vp[perm] = d["v_pages"]
+    p = gu.run_gpu(w, dict(d, k_pages=kp, v_pages=vp, block_table=perm.astype(np.int32)), cs, dev)
+    for key in ("k_rep", "sel_idx", "sel_cnt", "out", "scores"):
+        assert np.array_equal(a[key], p[key]), key
+
+
+def test_exact_ties_pick_lowest_index(dev):
+    """Duplicated K blocks give identical scores on the GPU too; the lowest indices win."""
+    w = SHAPES["gqa128"][0].with_(top_k=2)
+    gu.log("[parity] exact ties")
+    d = gen.make_layer(w)
+    cs = np.array([0, 12, 16], dtype=np.int32)
+    ref0 = _oracle(w, d, cs, with_output=False)
+    g = ref0["geometry"][1]
+    sc = ref0["scores"][1]
+    best = g.sink_blk + int(np.argmax(sc))
+    dups = [b for b in range(g.sink_blk, g.sink_blk + g.n_cand) if b != best][:3]
+    for b in dups:
+        d["k_pages"][b] = d["k_pages"][best]
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs, with_output=False)
+    tied = sorted(dups + [best])
+    assert list(ref["selections"][1]) == tied[:2]
+    assert list(res["sel_idx"][1, :2]) == tied[:2]
+
+
+@pytest.mark.parametrize("name,seed_rows", [("llama32k", 5), ("llama128k", 6)])
+def test_full_size_llama(dev, name, seed_rows):
+    """Full Llama-3-8B-layer workloads: every selection, and attention on sampled row tiles."""
+    w = gen.WORKLOADS[name]
+    gu.log(f"[parity] {name}: generating")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, w.cluster)
+    gu.log(f"[parity] {name}: GPU")
+    res = gu.run_gpu(w, d, cs, dev)
+    gu.log(f"[parity] {name}: oracle selection")
+    ref = _oracle(w, d, cs, with_output=False)
+    gu.check_rounding(res["k_rep"], ref["k_rep"], "k_rep")
+    gu.check_rounding(res["fingerprints"], np.stack(ref["fingerprints"]), "fingerprints")
+    worst = gu.check_scores(res["scores"], ref, w.num_kv_heads, name)
+    gu.log(f"[parity] {name}: worst score error {worst:.2e}")
+    n_exact = gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, EPS_VALID)
+    gu.log(f"[parity] {name}: {n_exact} of {len(cs) - 1} clusters above the margin, all equal")
+    assert res["calls"] == len(cs) - 1
+    rng = np.random.default_rng(seed_rows)
+    rows = gu.sample_rows(ref["geometry"], rng)
+    sels = gu.gpu_selections(res, len(cs) - 1)
+    worst = (0.0, 0.0)
+    for j, g in enumerate(ref["geometry"]):
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j], rows[j],
+                                      w.block_size)
+        mx, rel = gu.check_output(res["out"][rows[j]], o_ref, f"{name} cluster {j}")
+        worst = (max(worst[0], mx), max(worst[1], rel))
+    gu.log(f"[parity] {name}: sampled attention worst max-abs {worst[0]:.2e} rel-L2 {worst[1]:.2e}")
+
+
+def test_abi_errors_on_device(dev):
+    """Invalid calls on a live handle return their status and launch nothing."""
+    import ctypes
+
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = gen.WORKLOADS["tiny"]
+    cfg = gu.config(w, 2)
+    with pk.Scale(cfg) as h:
+        lib = pk.lib
+        buf = torch.zeros(1 << 20, dtype=torch.int32, device=dev)
+        p = buf.data_ptr()
+        cs = np.array([0, 4, 8], dtype=np.int32)
+        assert lib.scale_rep_keys(h.handle, p, None, 2048 + 64, p) == pk.SCALE_ERR_CAPACITY
+        assert lib.scale_rep_keys(h.handle, p, None, 100, p) == pk.SCALE_ERR_UNSUPPORTED
+        assert lib.scale_rep_keys(h.handle, None, None, 2048, p) == pk.SCALE_ERR_INVALID_ARG
+        big = np.array([0, 1, 2, 8], dtype=np.int32)
+        assert lib.scale_select_cluster(h.handle, p, 2048, p, big.ctypes.data, 3, p, p, None, None) == \
+            pk.SCALE_ERR_CAPACITY
+        bad = np.array([0, 5, 4], dtype=np.int32)
+        assert lib.scale_select_cluster(h.handle, p, 2048, p, bad.ctypes.data, 2, p, p, None, None) == \
+            pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_sparse_prefill(h.handle, p, p, p, None, 2048, cs.ctypes.data, 2, p, None, p) == \
+            pk.SCALE_ERR_INVALID_ARG
+        n = ctypes.c_int64()
+        assert lib.scale_retrieval_calls(h.handle, ctypes.byref(n)) == 0 and n.value == 0
+        torch.cuda.synchronize()
+        assert int(buf.abs().sum()) == 0
