@@ -64,7 +64,9 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
 // Row chunks of fingerprint_partial for a sub-chunk of `sub_chunk` rows.
 int fingerprint_chunks(int sub_chunk);
 
-// Positions per attention work item (query rows per KV head group of one work-group).
+// Query positions per attention work item for a group of `group` query heads per KV head
+// (a multiple of 32; at least kTilePositions).
+int attention_tile_positions(int group);
 constexpr int kTilePositions = 32;
 
 }  // namespace scale

@@ -349,26 +349,25 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
   WorkItem* items = reinterpret_cast<WorkItem*>(geo + n_clusters);
 
-  // Work list: (cluster, position tile) ordered by decreasing key count, each for every KV head.
+  // Work list. Clusters in order; inside a cluster, position tiles from the last (most keys) to
+  // the first; each tile once per KV head, KV head fastest. Work-groups are handed to the 8 XCDs
+  // round-robin, so a KV head stays on one XCD (and its L2) while the tiles of one cluster, which
+  // share the sink, selected and local K/V blocks, run together.
   const int B = c.block_size;
-  const int TP = scale::kTilePositions;
-  struct Tile { int64_t cost; int32_t cluster, p0, n_rows; };
-  std::vector<Tile> tiles;
-  tiles.reserve((size_t)(n_tokens / TP + n_clusters));
-  for (int j = 0; j < n_clusters; ++j) {
-    const ClusterGeo& g = geo[j];
-    for (int p0 = g.s; p0 < g.e; p0 += TP) {
-      const int nr = std::min(TP, g.e - p0);
-      const int64_t keys = (int64_t)(g.sink_eff + g.sel_cnt) * B + (p0 + nr - g.lo_blk * B);
-      tiles.push_back({keys, j, p0, nr});
-    }
-  }
-  std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& a, const Tile& b) { return a.cost > b.cost; });
-  const int64_t n_items = (int64_t)tiles.size() * c.num_kv_heads;
+  const int TP = scale::attention_tile_positions(c.num_q_heads / c.num_kv_heads);
+  int64_t n_items = 0;
+  for (int j = 0; j < n_clusters; ++j) n_items += (int64_t)((geo[j].e - geo[j].s + TP - 1) / TP) * c.num_kv_heads;
   if (n_items > h->max_items) return SCALE_ERR_CAPACITY;
   int64_t k = 0;
-  for (const Tile& t : tiles)
-    for (int g = 0; g < c.num_kv_heads; ++g) items[k++] = {t.cluster, g, t.p0, t.n_rows};
+  for (int j = 0; j < n_clusters; ++j) {
+    const ClusterGeo& g = geo[j];
+    const int n_tiles = (g.e - g.s + TP - 1) / TP;
+    for (int t = n_tiles - 1; t >= 0; --t) {
+      const int p0 = g.s + t * TP;
+      const int nr = std::min(TP, g.e - p0);
+      for (int kv = 0; kv < c.num_kv_heads; ++kv) items[k++] = {j, kv, p0, nr};
+    }
+  }
 
   // geometry and items sit back to back in the slot; they go to two device buffers
   if (hipMemcpyAsync(h->d_geo, geo, sizeof(ClusterGeo) * n_clusters, hipMemcpyHostToDevice, h->stream) != hipSuccess ||

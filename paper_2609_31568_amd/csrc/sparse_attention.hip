@@ -1,22 +1,39 @@
 // Gathered block-sparse flash attention for cluster-level sparse prefill (paper Sec. 5.1.3,
 // Eq. 10; Algorithm 2, "compute cluster attention ... with causal mask").
 //
-// Work item = (cluster j, KV head g, tile of up to 32 query positions). The work-group has one
-// wave per query head of the group (G = Hq / Hkv waves); all of them share every K/V tile that
-// is staged in LDS. The tile sequence of an item is: the sink blocks, the cluster's selected
-// blocks, then the local window [lo_blk * B, last position] in 64-key tiles; only the tile that
-// reaches the item's own positions needs the causal mask.
+// Work item = (cluster j, KV head g, tile of up to 32 * RB query positions). The work-group has
+// G * RB waves: one per (query head of the group, 32-position row block). All of them share the
+// K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds G * RB * 32 query rows. The
+// tile sequence of an item is: the sink blocks, the cluster's selected blocks, then the local
+// window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own positions
+// need the causal mask. The page of every tile is resolved once per item into an LDS table.
 //
 // Per 64-key tile and wave (d = head dim, 32 query rows of one head):
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q held in registers
-//   online softmax  fp32, base-2 exponent with the softmax scale folded into log2(e)
-//   O^T += V^T P^T  v_mfma_f32_32x32x16_bf16, A = V^T from LDS, B = P straight from the S^T
-//                   accumulators (bf16)
+//   online softmax  fp32 in base 2 with the softmax scale folded into one fma per score; the
+//                   reference max of a row is only raised when a tile exceeds it by more than
+//                   2^8 (exact: numerator and denominator share the reference; weights stay
+//                   <= 256), so the O rescale is rare
+//   O^T += V^T P^T  v_mfma_f32_32x32x16_bf16, A = V^T read from the key-major V tile with
+//                   ds_read_b64_tr_b16, B = P straight from the S^T accumulators (bf16)
 // Computing the transposed products keeps query row (lane % 32) in the same lanes for S, the
 // running max / sum and the O accumulators, so no LDS round trip is needed between the two
 // products. The key order inside a 16-key MFMA step is permuted consistently on both operands
 // (lane half 0 holds keys {0-3, 8-11}, lane half 1 keys {4-7, 12-15}), which is what the
 // accumulator layout of the first product hands to the second.
+//
+// ds_read_b64_tr_b16 (gfx950): within each group of 16 lanes, lane i receives element (i % 4)
+// of the 8-byte chunk addressed by lane 4e + i / 4, for e = 0..3. When lane L of the group
+// addresses V[key0 + L / 4][d0 + 4 (L % 4)], lane i gets V[key0 + e][d0 + i], e = 0..3: four
+// keys of one column, the A-operand slice of V^T.
+//
+// Pipelining: LDS holds two tile buffers. While a tile is consumed from one buffer, the next
+// tile's global loads are in flight into registers; they are written to the other buffer after
+// the MFMA work, and one barrier per tile separates the phases.
+//
+// LDS layouts (conflict-free for the operand reads and the tile writes):
+//   K [key][d], row stride d + 8 elements  (ds_read_b128: 8 lanes cover 8 rows, 32 banks)
+//   V [key][d], row stride d + 16 elements (ds_read_b64_tr_b16: 16 lanes cover 4 rows x 32 B)
 #include <math.h>
 
 #include "common.h"
@@ -27,40 +44,127 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr int kKeyTile = 64;                 // keys per LDS tile
-constexpr int kVtPad = 4;                    // V^T row padding (elements)
-constexpr int kKPad = 8;                     // K row padding (elements)
+constexpr int kKeyTile = 64;
+constexpr int kDescBatch = 256;       // tile descriptors resolved per batch
+constexpr float kRescaleLog2 = 8.0f;  // raise a row's reference max only past 2^8
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void sparse_attention_kernel(
+template <int D, int G, int RB>
+struct AttnShape {
+  static constexpr int kWaves = G * RB;
+  static constexpr int kThreads = kWaves * 64;
+  static constexpr int kKStride = D + 8;                   // elements
+  static constexpr int kVStride = D + 16;                  // elements
+  static constexpr int kKElems = kKeyTile * kKStride;
+  static constexpr int kVElems = kKeyTile * kVStride;
+  static constexpr int kBufElems = kKElems + kVElems;
+  static constexpr int kChunks = kKeyTile * D / 8;         // 16-byte chunks of one K or V tile
+  static constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
+};
+
+template <class S, int D>
+__device__ __forceinline__ void load_tile(u32x4 (&kreg)[S::kPer], u32x4 (&vreg)[S::kPer],
+                                          const uint16_t* __restrict__ k_pages,
+                                          const uint16_t* __restrict__ v_pages, int64_t base, int tid) {
+#pragma unroll
+  for (int i = 0; i < S::kPer; ++i) {
+    const int idx = tid + i * S::kThreads;
+    if (S::kChunks % S::kThreads == 0 || idx < S::kChunks) {
+      const int64_t off = base + (int64_t)(idx / (D / 8)) * D + 8 * (idx % (D / 8));
+      kreg[i] = *reinterpret_cast<const u32x4*>(k_pages + off);
+      vreg[i] = *reinterpret_cast<const u32x4*>(v_pages + off);
+    }
+  }
+}
+
+template <class S, int D>
+__device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u32x4 (&vreg)[S::kPer],
+                                           uint16_t* kl, int tid) {
+  uint16_t* vl = kl + S::kKElems;
+#pragma unroll
+  for (int i = 0; i < S::kPer; ++i) {
+    const int idx = tid + i * S::kThreads;
+    if (S::kChunks % S::kThreads == 0 || idx < S::kChunks) {
+      const int r = idx / (D / 8), c = idx % (D / 8);
+      *reinterpret_cast<u32x4*>(kl + r * S::kKStride + 8 * c) = kreg[i];
+      *reinterpret_cast<u32x4*>(vl + r * S::kVStride + 8 * c) = vreg[i];
+    }
+  }
+}
+
+template <int D, int G, int RB, int LOG2B>
+__global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pages,
     const uint16_t* __restrict__ v_pages, const int32_t* __restrict__ block_table,
     const ClusterGeo* __restrict__ geo, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt, int top_k,
-    int num_q_heads, int num_kv_heads, int block_size, int n_blocks, float qk_scale_log2,
-    int out_bf16, void* __restrict__ out) {
-  constexpr int kThreads = NW * 64;
-  constexpr int kKStride = D + kKPad;
-  constexpr int kVtStride = kKeyTile + kVtPad;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[kKeyTile * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * kVtStride];
+    int num_q_heads, int num_kv_heads, int n_blocks, float qk_scale_log2, int out_bf16,
+    void* __restrict__ out) {
+  using S = AttnShape<D, G, RB>;
+  constexpr int B = 1 << LOG2B;
+  constexpr int kTilesPerBlock = B / kKeyTile;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * S::kBufElems];
+  __shared__ int32_t tile_row[2][kDescBatch];   // first cache row ((page * Hkv + g) * B + off)
 
   const WorkItem it = items[blockIdx.x];
   const ClusterGeo cg = geo[it.cluster];
   const int g = it.kv_head;
-  const int wave = threadIdx.x / 64;
-  const int lane = threadIdx.x % 64;
+  const int tid = threadIdx.x;
+  const int wave = tid / 64;
+  const int lane = tid % 64;
   const int half = lane / 32;
   const int row = lane % 32;
-  const int h = g * NW + wave;
+  const int h = g * G + wave % G;
+  const int rb = wave / G;
   const int p0 = it.p0;
-  const int p = p0 + row;
-  const bool row_valid = row < it.n_rows;
+  const int wave_p0 = p0 + 32 * rb;
+  const int p = wave_p0 + row;
+  const bool row_valid = 32 * rb + row < it.n_rows;
 
-  // Q fragments: B operand of S^T = K Q^T for each 16-wide slice of d.
+  // ---- tile sequence: sink blocks, selected blocks, local window ----
+  int n_sel = sel_cnt[it.cluster];
+  n_sel = n_sel < 0 ? 0 : (n_sel > top_k ? top_k : n_sel);
+  const int n_sink_tiles = cg.sink_eff * kTilesPerBlock;
+  const int n_fixed = n_sink_tiles + n_sel * kTilesPerBlock;
+  const int local0 = cg.lo_blk << LOG2B;
+  const int local_end = p0 + it.n_rows;            // keys [local0, local_end) of the window
+  const int n_tiles = n_fixed + (local_end - local0 + kKeyTile - 1) / kKeyTile;
+  const int32_t* sel = sel_idx + (int64_t)it.cluster * top_k;
+
+  auto fill_batch = [&](int batch) {
+    const int t0 = batch * kDescBatch;
+    const int cnt = min(kDescBatch, n_tiles - t0);
+    for (int i = tid; i < cnt; i += S::kThreads) {
+      const int t = t0 + i;
+      int key0;
+      if (t < n_sink_tiles) {
+        key0 = t * kKeyTile;
+      } else if (t < n_fixed) {
+        const int u = t - n_sink_tiles;
+        int blk = sel[u / kTilesPerBlock];
+        blk = blk < 0 ? 0 : (blk >= n_blocks ? n_blocks - 1 : blk);
+        key0 = (blk << LOG2B) + (u % kTilesPerBlock) * kKeyTile;
+      } else {
+        key0 = local0 + (t - n_fixed) * kKeyTile;
+      }
+      const int blk = key0 >> LOG2B;
+      const int page = block_table ? block_table[blk] : blk;
+      tile_row[batch & 1][i] = ((page * num_kv_heads + g) << LOG2B) + (key0 & (B - 1));
+    }
+  };
+
+  // ---- per-thread prefetch registers for one K and one V tile ----
+  u32x4 kreg[S::kPer], vreg[S::kPer];
+#define SCALE_LOAD_TILE(T)                                                                       \
+  load_tile<S, D>(kreg, vreg, k_pages, v_pages,                                                  \
+                  (int64_t)tile_row[((T) / kDescBatch) & 1][(T) % kDescBatch] * D, tid)
+#define SCALE_STORE_TILE(BUF) store_tile<S, D>(kreg, vreg, lds + (BUF) * S::kBufElems, tid)
+
+  // ---- Q fragments: B operand of S^T = K Q^T for each 16-wide slice of d ----
   bf16x8 qf[D / 16];
   {
     const int pr = row_valid ? p : p0;
@@ -74,110 +178,85 @@ __global__ __launch_bounds__(NW * 64) void sparse_attention_kernel(
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
-  float m_run = -INFINITY;
-  float l_run = 0.f;
+  float m_ref = -INFINITY;   // reference max (raw score units) of this lane's row
+  float l_run = 0.f;         // this lane's share of the row's softmax denominator
 
-  const int tiles_per_block = block_size / kKeyTile;
-  int n_sel = sel_cnt[it.cluster];
-  n_sel = n_sel < 0 ? 0 : (n_sel > top_k ? top_k : n_sel);
-  const int n_sink_tiles = cg.sink_eff * tiles_per_block;
-  const int n_sel_tiles = n_sel * tiles_per_block;
-  const int local0 = cg.lo_blk * block_size;
-  const int local_end = p0 + it.n_rows;            // keys [local0, local_end) of the window
-  const int n_local_tiles = (local_end - local0 + kKeyTile - 1) / kKeyTile;
-  const int n_tiles = n_sink_tiles + n_sel_tiles + n_local_tiles;
-  const int32_t* sel = sel_idx + (int64_t)it.cluster * top_k;
+  // Per-lane LDS element offsets of the operand reads (immediate offsets add the rest).
+  const int k_off = row * S::kKStride + 8 * half;
+  const int li = lane % 16;
+  const int v_off = (4 * half + li / 4) * S::kVStride + 16 * ((lane / 16) % 2) + 4 * (li % 4);
+
+  fill_batch(0);
+  __syncthreads();
+  if (n_tiles > 0) {
+    SCALE_LOAD_TILE(0);
+    SCALE_STORE_TILE(0);
+  }
+  if (n_tiles > kDescBatch) fill_batch(1);
+  __syncthreads();
 
   for (int t = 0; t < n_tiles; ++t) {
-    int key0;
-    if (t < n_sink_tiles) {
-      key0 = t * kKeyTile;
-    } else if (t < n_sink_tiles + n_sel_tiles) {
-      const int u = t - n_sink_tiles;
-      int blk = sel[u / tiles_per_block];
-      blk = blk < 0 ? 0 : (blk >= n_blocks ? n_blocks - 1 : blk);
-      key0 = blk * block_size + (u % tiles_per_block) * kKeyTile;
-    } else {
-      key0 = local0 + (t - n_sink_tiles - n_sel_tiles) * kKeyTile;
-    }
-    const int blk = key0 / block_size;
-    const int page = block_table ? block_table[blk] : blk;
-    const int64_t base = (((int64_t)page * num_kv_heads + g) * block_size + (key0 - blk * block_size)) * D;
-    const uint16_t* kt = k_pages + base;
-    const uint16_t* vt = v_pages + base;
+    const int buf = t & 1;
+    if (t > 0 && t % kDescBatch == 0 && t + kDescBatch < n_tiles) fill_batch(t / kDescBatch + 1);
+    if (t + 1 < n_tiles) SCALE_LOAD_TILE(t + 1);
 
-    __syncthreads();   // every wave is done with the previous tile
-    // K tile: [key][d] rows of 16-byte chunks.
-    for (int i = threadIdx.x; i < kKeyTile * D / 8; i += kThreads) {
-      const int r = i / (D / 8), c = i % (D / 8);
-      *reinterpret_cast<uint4*>(k_lds + r * kKStride + 8 * c) =
-          *reinterpret_cast<const uint4*>(kt + (int64_t)r * D + 8 * c);
-    }
-    // V tile transposed: [d][key], two keys per 32-bit store.
-    for (int i = threadIdx.x; i < (kKeyTile / 2) * (D / 8); i += kThreads) {
-      const int c = i % (D / 8), kp = i / (D / 8);
-      const uint4 a = *reinterpret_cast<const uint4*>(vt + (int64_t)(2 * kp) * D + 8 * c);
-      const uint4 b = *reinterpret_cast<const uint4*>(vt + (int64_t)(2 * kp + 1) * D + 8 * c);
-      const uint32_t wa[4] = {a.x, a.y, a.z, a.w};
-      const uint32_t wb[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        uint32_t* dst0 = reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * e) * kVtStride + 2 * kp);
-        uint32_t* dst1 = reinterpret_cast<uint32_t*>(vt_lds + (8 * c + 2 * e + 1) * kVtStride + 2 * kp);
-        *dst0 = (wa[e] & 0xFFFFu) | (wb[e] << 16);
-        *dst1 = (wa[e] >> 16) | (wb[e] & 0xFFFF0000u);
-      }
-    }
-    __syncthreads();
+    const uint16_t* k_lds = lds + buf * S::kBufElems;
+    const uint16_t* v_lds = k_lds + S::kKElems;
 
     // S^T for the two 32-key halves of the tile.
     f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      const uint16_t* krow = k_lds + k_off + 32 * kb * S::kKStride;
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow), qf[0],
+                                                      f32x16{}, 0, 0, 0);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[kb][e] = 0.f;
-      const uint16_t* krow = k_lds + (32 * kb + row) * kKStride + 8 * half;
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + 16 * c);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[c], s[kb], 0, 0, 0);
-      }
+      for (int c = 1; c < D / 16; ++c)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * c), qf[c],
+                                                        s[kb], 0, 0, 0);
     }
 
-    // Scale into base 2, causal mask on the tile that reaches this item's positions.
-    const bool diag = key0 + kKeyTile > p0;
-    float mt = -INFINITY;
+    // Causal mask only on a local tile that reaches this wave's positions.
+    if (t >= n_fixed) {
+      const int key0 = local0 + (t - n_fixed) * kKeyTile;
+      if (key0 + kKeyTile > wave_p0) {
+        const int lim = p - key0 - 4 * half;     // mask key offsets above this
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (32 * kb + 8 * (e / 4) + (e % 4) > lim) s[kb][e] = -INFINITY;
+      }
+    }
+    float mt = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float x = s[kb][e] * qk_scale_log2;
-        if (diag) {
-          const int key = key0 + 32 * kb + 8 * (e / 4) + 4 * half + (e % 4);
-          if (key > p) x = -INFINITY;
-        }
-        s[kb][e] = x;
-        mt = fmaxf(mt, x);
-      }
+      for (int e = (kb == 0 ? 2 : 0); e < 16; ++e) mt = fmaxf(mt, s[kb][e]);
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    float psum = 0.f;
+    if (__any((mt - m_ref) * qk_scale_log2 > kRescaleLog2)) {
+      const float m_new = fmaxf(m_ref, mt);
+      const float alpha = m_new == -INFINITY ? 1.f : fast_exp2((m_ref - m_new) * qk_scale_log2);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+      m_ref = m_new;
+    }
+    const float mc = m_ref == -INFINITY ? 0.f : m_ref * qk_scale_log2;
+    float ps[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ps[i] = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float pv = fast_exp2(s[kb][e] - m_use);
+        const float pv = fast_exp2(fmaf(s[kb][e], qk_scale_log2, -mc));
         s[kb][e] = pv;
-        psum += pv;
+        ps[e % 8] += pv;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+    l_run += ((ps[0] + ps[1]) + (ps[2] + ps[3])) + ((ps[4] + ps[5]) + (ps[6] + ps[7]));
 
     // P fragments: key chunk kc = 2 kb + u takes accumulator entries [8u, 8u + 8) of s[kb].
     bf16x8 pf[4];
@@ -186,19 +265,27 @@ __global__ __launch_bounds__(NW * 64) void sparse_attention_kernel(
 #pragma unroll
       for (int e = 0; e < 8; ++e) pf[kc][e] = (__bf16)s[kc / 2][8 * (kc % 2) + e];
 
-    // O^T += V^T P^T
+    // O^T += V^T P^T; the two transposing reads give keys {16kc + 4half + 0..3} and
+    // {16kc + 8 + 4half + 0..3} of column 32 db + lane % 32.
+    const uint16_t* vbase = v_lds + v_off;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const uint16_t* vrow = vt_lds + (32 * db + row) * kVtStride + 4 * half;
 #pragma unroll
       for (int kc = 0; kc < 4; ++kc) {
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow + 16 * kc);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16 * kc + 8);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vbase + (16 * kc) * S::kVStride + 32 * db));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vbase + (16 * kc + 8) * S::kVStride + 32 * db));
         const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kc], o[db], 0, 0, 0);
       }
     }
+
+    if (t + 1 < n_tiles) SCALE_STORE_TILE(buf ^ 1);
+    __syncthreads();
   }
+#undef SCALE_LOAD_TILE
+#undef SCALE_STORE_TILE
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
@@ -220,45 +307,55 @@ __global__ __launch_bounds__(NW * 64) void sparse_attention_kernel(
     }
 }
 
-template <int D, int NW>
-hipError_t launch_nw(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
-                     const int32_t* block_table, const ClusterGeo* geo, const WorkItem* items,
-                     int n_items, const int32_t* sel_idx, const int32_t* sel_cnt, int top_k,
-                     int num_q_heads, int num_kv_heads, int block_size, int n_blocks,
-                     float qk_scale_log2, int out_bf16, void* out, hipStream_t stream) {
-  sparse_attention_kernel<D, NW><<<n_items, NW * 64, 0, stream>>>(
-      q, k_pages, v_pages, block_table, geo, items, sel_idx, sel_cnt, top_k, num_q_heads, num_kv_heads,
-      block_size, n_blocks, qk_scale_log2, out_bf16, out);
+// Row blocks per query head for a group of G query heads: up to 8 waves per work-group.
+constexpr int row_blocks(int group) { return group >= 8 ? 1 : (8 / group); }
+
+struct LaunchArgs {
+  const uint16_t *q, *k_pages, *v_pages;
+  const int32_t* block_table;
+  const ClusterGeo* geo;
+  const WorkItem* items;
+  int n_items;
+  const int32_t *sel_idx, *sel_cnt;
+  int top_k, num_q_heads, num_kv_heads, n_blocks;
+  float qk_scale_log2;
+  int out_bf16;
+  void* out;
+  hipStream_t stream;
+};
+
+template <int D, int G, int LOG2B>
+hipError_t launch_dgb(const LaunchArgs& a) {
+  constexpr int RB = row_blocks(G);
+  sparse_attention_kernel<D, G, RB, LOG2B><<<a.n_items, G * RB * 64, 0, a.stream>>>(
+      a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
+      a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out);
   return hipGetLastError();
 }
 
+template <int D, int G>
+hipError_t launch_dg(int block_size, const LaunchArgs& a) {
+  return block_size == 128 ? launch_dgb<D, G, 7>(a) : launch_dgb<D, G, 6>(a);
+}
+
 template <int D>
-hipError_t launch_d(int group, const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
-                    const int32_t* block_table, const ClusterGeo* geo, const WorkItem* items, int n_items,
-                    const int32_t* sel_idx, const int32_t* sel_cnt, int top_k, int num_q_heads,
-                    int num_kv_heads, int block_size, int n_blocks, float qk_scale_log2, int out_bf16,
-                    void* out, hipStream_t stream) {
-#define SCALE_NW_CASE(NWV)                                                                              \
-  case NWV:                                                                                            \
-    return launch_nw<D, NWV>(q, k_pages, v_pages, block_table, geo, items, n_items, sel_idx, sel_cnt,  \
-                             top_k, num_q_heads, num_kv_heads, block_size, n_blocks, qk_scale_log2,    \
-                             out_bf16, out, stream);
+hipError_t launch_d(int group, int block_size, const LaunchArgs& a) {
   switch (group) {
-    SCALE_NW_CASE(1)
-    SCALE_NW_CASE(2)
-    SCALE_NW_CASE(3)
-    SCALE_NW_CASE(4)
-    SCALE_NW_CASE(5)
-    SCALE_NW_CASE(6)
-    SCALE_NW_CASE(7)
-    SCALE_NW_CASE(8)
-    default:
-      return hipErrorInvalidValue;
+    case 1: return launch_dg<D, 1>(block_size, a);
+    case 2: return launch_dg<D, 2>(block_size, a);
+    case 3: return launch_dg<D, 3>(block_size, a);
+    case 4: return launch_dg<D, 4>(block_size, a);
+    case 5: return launch_dg<D, 5>(block_size, a);
+    case 6: return launch_dg<D, 6>(block_size, a);
+    case 7: return launch_dg<D, 7>(block_size, a);
+    case 8: return launch_dg<D, 8>(block_size, a);
+    default: return hipErrorInvalidValue;
   }
-#undef SCALE_NW_CASE
 }
 
 }  // namespace
+
+int attention_tile_positions(int group) { return 32 * row_blocks(group); }
 
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
@@ -267,12 +364,10 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
+  const LaunchArgs a{q, k_pages, v_pages, block_table, geo, items, n_items, sel_idx, sel_cnt, top_k,
+                     num_q_heads, num_kv_heads, n_blocks, qk_scale_log2, out_bf16, out, stream};
   const int group = num_q_heads / num_kv_heads;
-  if (head_dim == 128)
-    return launch_d<128>(group, q, k_pages, v_pages, block_table, geo, items, n_items, sel_idx, sel_cnt, top_k,
-                         num_q_heads, num_kv_heads, block_size, n_blocks, qk_scale_log2, out_bf16, out, stream);
-  return launch_d<64>(group, q, k_pages, v_pages, block_table, geo, items, n_items, sel_idx, sel_cnt, top_k,
-                      num_q_heads, num_kv_heads, block_size, n_blocks, qk_scale_log2, out_bf16, out, stream);
+  return head_dim == 128 ? launch_d<128>(group, block_size, a) : launch_d<64>(group, block_size, a);
 }
 
 }  // namespace scale

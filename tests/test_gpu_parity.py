@@ -147,6 +147,26 @@ def test_exact_ties_pick_lowest_index(dev):
     assert list(res["sel_idx"][1, :2]) == tied[:2]
 
 
+def test_items_with_more_than_256_tiles(dev):
+    """A window of 18000 tokens: late work items walk more than 256 key tiles, so the kernel's tile
+    table is refilled mid-item. Checked on sampled rows of every cluster."""
+    w = gen.Workload("wide", 1, 4, 1, 64, 20480, 64, 512, 2, 4, 64, 18000, 10, 1, 3, 41)
+    gu.log("[parity] wide window")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 2)
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs, with_output=False)
+    gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, EPS_VALID)
+    last = ref["geometry"][-1]
+    assert (last.e - last.lo_blk * w.block_size) // 64 > 256
+    rows = gu.sample_rows(ref["geometry"], np.random.default_rng(9), tiles_per_cluster=2)
+    sels = gu.gpu_selections(res, len(cs) - 1)
+    for j, g in enumerate(ref["geometry"]):
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j], rows[j],
+                                      w.block_size)
+        gu.check_output(res["out"][rows[j]], o_ref, f"wide cluster {j}")
+
+
 @pytest.mark.parametrize("name,seed_rows", [("llama32k", 5), ("llama128k", 6)])
 def test_full_size_llama(dev, name, seed_rows):
     """Full Llama-3-8B-layer workloads: every selection, and attention on sampled row tiles."""
