@@ -65,8 +65,10 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
 int fingerprint_chunks(int sub_chunk);
 
 // Query positions per attention work item for a group of `group` query heads per KV head
-// (a multiple of 32; at least kTilePositions).
+// (a multiple of kTilePositions), and the number of head groups one KV head's query heads are
+// split into. WorkItem.kv_head carries the KV head in its low 16 bits and the head group above.
 int attention_tile_positions(int group);
+int attention_head_groups(int group);
 constexpr int kTilePositions = 32;
 
 }  // namespace scale

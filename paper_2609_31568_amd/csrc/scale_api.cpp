@@ -5,7 +5,7 @@
 // cluster geometry and the attention work list) is written into a ring of pinned host slots and
 // copied to device scratch asynchronously on the handle's stream; a slot is reused only after
 // the event recorded behind its copy has completed.
-#include "../../include/scale.h"
+#include "scale.h"
 
 #include <hip/hip_runtime.h>
 
@@ -115,7 +115,7 @@ scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_
 
 int64_t max_work_items(const scale_config& c) {
   const int64_t tiles = ((int64_t)c.max_tokens + scale::kTilePositions - 1) / scale::kTilePositions + c.max_clusters;
-  return tiles * c.num_kv_heads;
+  return tiles * c.num_kv_heads * scale::attention_head_groups(c.num_q_heads / c.num_kv_heads);
 }
 
 hipEvent_t take_event(scale_ctx* h) {
@@ -354,9 +354,12 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   // round-robin, so a KV head stays on one XCD (and its L2) while the tiles of one cluster, which
   // share the sink, selected and local K/V blocks, run together.
   const int B = c.block_size;
-  const int TP = scale::attention_tile_positions(c.num_q_heads / c.num_kv_heads);
+  const int group = c.num_q_heads / c.num_kv_heads;
+  const int TP = scale::attention_tile_positions(group);
+  const int HG = scale::attention_head_groups(group);
   int64_t n_items = 0;
-  for (int j = 0; j < n_clusters; ++j) n_items += (int64_t)((geo[j].e - geo[j].s + TP - 1) / TP) * c.num_kv_heads;
+  for (int j = 0; j < n_clusters; ++j)
+    n_items += (int64_t)((geo[j].e - geo[j].s + TP - 1) / TP) * c.num_kv_heads * HG;
   if (n_items > h->max_items) return SCALE_ERR_CAPACITY;
   int64_t k = 0;
   for (int j = 0; j < n_clusters; ++j) {
@@ -365,7 +368,8 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
     for (int t = n_tiles - 1; t >= 0; --t) {
       const int p0 = g.s + t * TP;
       const int nr = std::min(TP, g.e - p0);
-      for (int kv = 0; kv < c.num_kv_heads; ++kv) items[k++] = {j, kv, p0, nr};
+      for (int kv = 0; kv < c.num_kv_heads; ++kv)
+        for (int hg = 0; hg < HG; ++hg) items[k++] = {j, kv | (hg << 16), p0, nr};
     }
   }
 

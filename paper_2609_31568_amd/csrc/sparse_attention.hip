@@ -10,10 +10,11 @@
 //
 // Per 64-key tile and wave (d = head dim, 32 query rows of one head):
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q held in registers
-//   online softmax  fp32 in base 2 with the softmax scale folded into one fma per score; the
-//                   reference max of a row is only raised when a tile exceeds it by more than
-//                   2^8 (exact: numerator and denominator share the reference; weights stay
-//                   <= 256), so the O rescale is rare
+//   online softmax  fp32 in base 2 with the softmax scale folded into one fma per score. A
+//                   row keeps a reference max that is only raised when a half tile's weights
+//                   against it would sum past 2^20 (exact: numerator and denominator share the
+//                   reference); no per-tile max is taken, the bf16 weight sum is the check, and
+//                   the O rescale is rare
 //   O^T += V^T P^T  v_mfma_f32_32x32x16_bf16, A = V^T read from the key-major V tile with
 //                   ds_read_b64_tr_b16, B = P straight from the S^T accumulators (bf16)
 // Computing the transposed products keeps query row (lane % 32) in the same lanes for S, the
@@ -26,6 +27,11 @@
 // of the 8-byte chunk addressed by lane 4e + i / 4, for e = 0..3. When lane L of the group
 // addresses V[key0 + L / 4][d0 + 4 (L % 4)], lane i gets V[key0 + e][d0 + i], e = 0..3: four
 // keys of one column, the A-operand slice of V^T.
+//
+// Order inside a tile: S(keys 0-31), S(keys 32-63), softmax(0-31), PV(0-31), softmax(32-63),
+// PV(32-63). MFMAs run asynchronously, so each half's VALU softmax overlaps the MFMAs issued
+// just before it (the other half's S, then the first half's PV) within the wave; the second wave
+// on the SIMD fills what is left.
 //
 // Pipelining: LDS holds two tile buffers. While a tile is consumed from one buffer, the next
 // tile's global loads are in flight into registers; they are written to the other buffer after
@@ -49,9 +55,27 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int kKeyTile = 64;
 constexpr int kDescBatch = 256;       // tile descriptors resolved per batch
-constexpr float kRescaleLog2 = 8.0f;  // raise a row's reference max only past 2^8
+constexpr float kWeightSumLimit = 1048576.0f;   // 2^20: bound on a lane's weight sum per half tile
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Weights of one 32-key half against reference mc (= m_ref * c): p = 2^(s c - mc) rounded to
+// bf16 into the two P fragments of the half; returns the lane's sum of the bf16 weights.
+__device__ __forceinline__ float half_weights(const f32x16& s, float mc, float c, bf16x8 (&pf)[2]) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+  for (int e = 0; e < 16; e += 2) {
+    const bf16x2 w = {(__bf16)fast_exp2(fmaf(s[e], c, -mc)), (__bf16)fast_exp2(fmaf(s[e + 1], c, -mc))};
+    pf[e / 8][e % 8] = w[0];
+    pf[e / 8][e % 8 + 1] = w[1];
+    if (e & 2) acc1 = __builtin_amdgcn_fdot2_f32_bf16(w, ones, acc1, false);
+    else acc0 = __builtin_amdgcn_fdot2_f32_bf16(w, ones, acc0, false);
+  }
+  return acc0 + acc1;
+}
 
 template <int D, int G, int RB>
 struct AttnShape {
@@ -112,7 +136,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
   const WorkItem it = items[blockIdx.x];
   const ClusterGeo cg = geo[it.cluster];
-  const int g = it.kv_head;
+  const int g = it.kv_head & 0xFFFF;
   const int tid = threadIdx.x;
   const int wave = tid / 64;
   const int lane = tid % 64;
@@ -178,7 +202,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[db][e] = 0.f;
-  float m_ref = -INFINITY;   // reference max (raw score units) of this lane's row
+  float m_ref = -1e30f;      // reference max (raw score units) of this lane's row
   float l_run = 0.f;         // this lane's share of the row's softmax denominator
 
   // Per-lane LDS element offsets of the operand reads (immediate offsets add the rest).
@@ -228,56 +252,47 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
             if (32 * kb + 8 * (e / 4) + (e % 4) > lim) s[kb][e] = -INFINITY;
       }
     }
-    float mt = fmaxf(s[0][0], s[0][1]);
+    // Softmax and PV one 32-key half at a time. Weights are first taken against the row's
+    // reference max; their bf16 sum (v_dot2 with ones) doubles as the overflow check: a sum
+    // above 2^20 (or inf / NaN) means a score exceeded the reference by about 2^15 or more, and
+    // the half is redone exactly (true max, O and denominator rescaled). The first tile always
+    // takes that path, since the reference starts at -1e30.
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 pf[2];
+      float lsum = half_weights(s[kb], m_ref * qk_scale_log2, qk_scale_log2, pf);
+      if (__any(!(lsum <= kWeightSumLimit))) {
+        float mt = fmaxf(s[kb][0], s[kb][1]);
 #pragma unroll
-      for (int e = (kb == 0 ? 2 : 0); e < 16; ++e) mt = fmaxf(mt, s[kb][e]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    if (__any((mt - m_ref) * qk_scale_log2 > kRescaleLog2)) {
-      const float m_new = fmaxf(m_ref, mt);
-      const float alpha = m_new == -INFINITY ? 1.f : fast_exp2((m_ref - m_new) * qk_scale_log2);
-      l_run *= alpha;
+        for (int e = 2; e < 16; ++e) mt = fmaxf(mt, s[kb][e]);
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        const float m_new = fmaxf(m_ref, mt);
+        const float alpha = fast_exp2((m_ref - m_new) * qk_scale_log2);
+        l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+        for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
-      m_ref = m_new;
-    }
-    const float mc = m_ref == -INFINITY ? 0.f : m_ref * qk_scale_log2;
-    float ps[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) ps[i] = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float pv = fast_exp2(fmaf(s[kb][e], qk_scale_log2, -mc));
-        s[kb][e] = pv;
-        ps[e % 8] += pv;
+          for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
+        m_ref = m_new;
+        lsum = half_weights(s[kb], m_ref * qk_scale_log2, qk_scale_log2, pf);
       }
-    l_run += ((ps[0] + ps[1]) + (ps[2] + ps[3])) + ((ps[4] + ps[5]) + (ps[6] + ps[7]));
+      l_run += lsum;
 
-    // P fragments: key chunk kc = 2 kb + u takes accumulator entries [8u, 8u + 8) of s[kb].
-    bf16x8 pf[4];
+      // O^T += V^T P^T over this half's two 16-key chunks; the transposing reads give keys
+      // {16kc + 4half + 0..3} and {16kc + 8 + 4half + 0..3} of column 32 db + lane % 32.
+      const uint16_t* vbase = v_lds + v_off;
 #pragma unroll
-    for (int kc = 0; kc < 4; ++kc)
+      for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pf[kc][e] = (__bf16)s[kc / 2][8 * (kc % 2) + e];
-
-    // O^T += V^T P^T; the two transposing reads give keys {16kc + 4half + 0..3} and
-    // {16kc + 8 + 4half + 0..3} of column 32 db + lane % 32.
-    const uint16_t* vbase = v_lds + v_off;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
-        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vbase + (16 * kc) * S::kVStride + 32 * db));
-        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (lds_bf16x4*)(vbase + (16 * kc + 8) * S::kVStride + 32 * db));
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kc], o[db], 0, 0, 0);
+        for (int u = 0; u < 2; ++u) {
+          const int kc = 2 * kb + u;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(vbase + (16 * kc) * S::kVStride + 32 * db));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(vbase + (16 * kc + 8) * S::kVStride + 32 * db));
+          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[u], o[db], 0, 0, 0);
+        }
       }
     }
 
@@ -356,6 +371,7 @@ hipError_t launch_d(int group, int block_size, const LaunchArgs& a) {
 }  // namespace
 
 int attention_tile_positions(int group) { return 32 * row_blocks(group); }
+int attention_head_groups(int) { return 1; }   // one work-group covers every query head of a KV head
 
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
