@@ -15,18 +15,13 @@
 //                   against it would sum past 2^20 (exact: numerator and denominator share the
 //                   reference); no per-tile max is taken, the bf16 weight sum is the check, and
 //                   the O rescale is rare
-//   O^T += V^T P^T  v_mfma_f32_32x32x16_bf16, A = V^T read from the key-major V tile with
-//                   ds_read_b64_tr_b16, B = P straight from the S^T accumulators (bf16)
+//   O^T += V^T P^T  v_mfma_f32_32x32x16_bf16, A = V^T from LDS (ds_read_b128), B = P straight
+//                   from the S^T accumulators (bf16)
 // Computing the transposed products keeps query row (lane % 32) in the same lanes for S, the
 // running max / sum and the O accumulators, so no LDS round trip is needed between the two
-// products. The key order inside a 16-key MFMA step is permuted consistently on both operands
-// (lane half 0 holds keys {0-3, 8-11}, lane half 1 keys {4-7, 12-15}), which is what the
-// accumulator layout of the first product hands to the second.
-//
-// ds_read_b64_tr_b16 (gfx950): within each group of 16 lanes, lane i receives element (i % 4)
-// of the 8-byte chunk addressed by lane 4e + i / 4, for e = 0..3. When lane L of the group
-// addresses V[key0 + L / 4][d0 + 4 (L % 4)], lane i gets V[key0 + e][d0 + i], e = 0..3: four
-// keys of one column, the A-operand slice of V^T.
+// products. K rows are stored in LDS in a permuted order so that the S^T accumulators of lane half
+// h hold the 16 consecutive keys [16h, 16h + 16) of each 32-key block; a 16-key PV step then takes
+// 8 consecutive keys from each lane half, which the V^T operand reads as one 16-byte chunk.
 //
 // Order inside a tile: S(keys 0-31), S(keys 32-63), softmax(0-31), PV(0-31), softmax(32-63),
 // PV(32-63). MFMAs run asynchronously, so each half's VALU softmax overlaps the MFMAs issued
@@ -38,8 +33,12 @@
 // the MFMA work, and one barrier per tile separates the phases.
 //
 // LDS layouts (conflict-free for the operand reads and the tile writes):
-//   K [key][d], row stride d + 8 elements  (ds_read_b128: 8 lanes cover 8 rows, 32 banks)
-//   V [key][d], row stride d + 16 elements (ds_read_b64_tr_b16: 16 lanes cover 4 rows x 32 B)
+//   K   [row][d], row stride d + 8 elements; row 32 b + 8 i + 4 h + j holds key 32 b + 16 h + 4 i + j
+//   V^T [d][key], row stride 68 dwords; the 32 key-pair dwords of row d start at dword
+//       4 ((d / 8) % 8), so the transposing 32-bit writes of a 32-lane group (4 key pairs x 8
+//       d-chunks) hit 32 banks, and the 16-byte reads of 8 lanes (8 rows) do too.
+// (ds_read_b64_tr_b16 would avoid the transposing writes, but it sustains well under half the
+// bytes per clock of ds_read_b128, and the V operand reads dominate the LDS traffic.)
 #include <math.h>
 
 #include "common.h"
@@ -82,40 +81,80 @@ struct AttnShape {
   static constexpr int kWaves = G * RB;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKStride = D + 8;                   // elements
-  static constexpr int kVStride = D + 16;                  // elements
+  static constexpr int kVtStrideDw = 68;                   // dwords per V^T row
   static constexpr int kKElems = kKeyTile * kKStride;
-  static constexpr int kVElems = kKeyTile * kVStride;
+  static constexpr int kVElems = D * kVtStrideDw * 2;
   static constexpr int kBufElems = kKElems + kVElems;
-  static constexpr int kChunks = kKeyTile * D / 8;         // 16-byte chunks of one K or V tile
+  static constexpr int kChunks = kKeyTile * D / 8;         // 16-byte chunks of one K tile
   static constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
+  static constexpr int kVUnits = (kKeyTile / 2) * (D / 8); // (key pair, 8-wide d chunk) units
+  static constexpr int kVPer = (kVUnits + kThreads - 1) / kThreads;
 };
 
+// LDS row of tile key r: the permutation that makes lane half h of the S^T accumulators hold
+// keys [16h, 16h + 16) of its 32-key block.
+__device__ __forceinline__ int k_lds_row(int r) {
+  const int k = r & 31;
+  return (r & 32) + 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3);
+}
+
+// V unit u = (key pair kp, d chunk c): lanes of a 32-lane group cover 8 consecutive chunks of 4 key
+// pairs (coalesced 128-byte global reads, conflict-free transposing LDS writes).
+template <int D>
+__device__ __forceinline__ void v_unit(int u, int& kp, int& c) {
+  const int rest = u >> 5;
+  c = (u & 7) + 8 * (rest % (D / 64));
+  kp = 4 * (rest / (D / 64)) + ((u >> 3) & 3);
+}
+
 template <class S, int D>
-__device__ __forceinline__ void load_tile(u32x4 (&kreg)[S::kPer], u32x4 (&vreg)[S::kPer],
+__device__ __forceinline__ void load_tile(u32x4 (&kreg)[S::kPer], u32x4 (&vreg)[2 * S::kVPer],
                                           const uint16_t* __restrict__ k_pages,
                                           const uint16_t* __restrict__ v_pages, int64_t base, int tid) {
 #pragma unroll
   for (int i = 0; i < S::kPer; ++i) {
     const int idx = tid + i * S::kThreads;
-    if (S::kChunks % S::kThreads == 0 || idx < S::kChunks) {
-      const int64_t off = base + (int64_t)(idx / (D / 8)) * D + 8 * (idx % (D / 8));
-      kreg[i] = *reinterpret_cast<const u32x4*>(k_pages + off);
-      vreg[i] = *reinterpret_cast<const u32x4*>(v_pages + off);
+    if (S::kChunks % S::kThreads == 0 || idx < S::kChunks)
+      kreg[i] = *reinterpret_cast<const u32x4*>(k_pages + base + (int64_t)(idx / (D / 8)) * D + 8 * (idx % (D / 8)));
+  }
+#pragma unroll
+  for (int i = 0; i < S::kVPer; ++i) {
+    const int u = tid + i * S::kThreads;
+    if (S::kVUnits % S::kThreads == 0 || u < S::kVUnits) {
+      int kp, c;
+      v_unit<D>(u, kp, c);
+      const uint16_t* src = v_pages + base + (int64_t)(2 * kp) * D + 8 * c;
+      vreg[2 * i] = *reinterpret_cast<const u32x4*>(src);
+      vreg[2 * i + 1] = *reinterpret_cast<const u32x4*>(src + D);
     }
   }
 }
 
 template <class S, int D>
-__device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u32x4 (&vreg)[S::kPer],
+__device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u32x4 (&vreg)[2 * S::kVPer],
                                            uint16_t* kl, int tid) {
-  uint16_t* vl = kl + S::kKElems;
+  uint32_t* vt = reinterpret_cast<uint32_t*>(kl + S::kKElems);
 #pragma unroll
   for (int i = 0; i < S::kPer; ++i) {
     const int idx = tid + i * S::kThreads;
     if (S::kChunks % S::kThreads == 0 || idx < S::kChunks) {
       const int r = idx / (D / 8), c = idx % (D / 8);
-      *reinterpret_cast<u32x4*>(kl + r * S::kKStride + 8 * c) = kreg[i];
-      *reinterpret_cast<u32x4*>(vl + r * S::kVStride + 8 * c) = vreg[i];
+      *reinterpret_cast<u32x4*>(kl + k_lds_row(r) * S::kKStride + 8 * c) = kreg[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < S::kVPer; ++i) {
+    const int u = tid + i * S::kThreads;
+    if (S::kVUnits % S::kThreads == 0 || u < S::kVUnits) {
+      int kp, c;
+      v_unit<D>(u, kp, c);
+      const u32x4 a = vreg[2 * i], b = vreg[2 * i + 1];   // keys 2kp and 2kp+1, d = 8c .. 8c+7
+      uint32_t* dst = vt + (8 * c) * S::kVtStrideDw + 4 * (c & 7) + kp;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dst[(2 * e) * S::kVtStrideDw] = (a[e] & 0xFFFFu) | (b[e] << 16);
+        dst[(2 * e + 1) * S::kVtStrideDw] = (a[e] >> 16) | (b[e] & 0xFFFF0000u);
+      }
     }
   }
 }
@@ -182,7 +221,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   };
 
   // ---- per-thread prefetch registers for one K and one V tile ----
-  u32x4 kreg[S::kPer], vreg[S::kPer];
+  u32x4 kreg[S::kPer], vreg[2 * S::kVPer];
 #define SCALE_LOAD_TILE(T)                                                                       \
   load_tile<S, D>(kreg, vreg, k_pages, v_pages,                                                  \
                   (int64_t)tile_row[((T) / kDescBatch) & 1][(T) % kDescBatch] * D, tid)
@@ -207,8 +246,13 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
   // Per-lane LDS element offsets of the operand reads (immediate offsets add the rest).
   const int k_off = row * S::kKStride + 8 * half;
-  const int li = lane % 16;
-  const int v_off = (4 * half + li / 4) * S::kVStride + 16 * ((lane / 16) % 2) + 4 * (li % 4);
+  // V^T row 32 db + row starts its keys at dword 4 ((32 db + row) / 8 % 8); lane half h reads keys
+  // 16h + [0, 16) of each 32-key block, the 16-byte chunk of keys 32 kb + 16 h + 8 u at dword
+  // offset 16 kb + 8 h + 4 u.
+  int vt_off[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+    vt_off[db] = 2 * ((32 * db + row) * S::kVtStrideDw + 4 * ((4 * db + row / 8) & 7) + 8 * half);
 
   fill_batch(0);
   __syncthreads();
@@ -244,12 +288,12 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     if (t >= n_fixed) {
       const int key0 = local0 + (t - n_fixed) * kKeyTile;
       if (key0 + kKeyTile > wave_p0) {
-        const int lim = p - key0 - 4 * half;     // mask key offsets above this
+        const int lim = p - key0 - 16 * half;    // accumulator e of block kb is key 32kb + 16half + e
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (32 * kb + 8 * (e / 4) + (e % 4) > lim) s[kb][e] = -INFINITY;
+            if (32 * kb + e > lim) s[kb][e] = -INFINITY;
       }
     }
     // Softmax and PV one 32-key half at a time. Weights are first taken against the row's
@@ -278,19 +322,13 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
       }
       l_run += lsum;
 
-      // O^T += V^T P^T over this half's two 16-key chunks; the transposing reads give keys
-      // {16kc + 4half + 0..3} and {16kc + 8 + 4half + 0..3} of column 32 db + lane % 32.
-      const uint16_t* vbase = v_lds + v_off;
+      // O^T += V^T P^T over this half's two 16-key steps: step u takes keys 32kb + 16h + 8u + [0, 8)
+      // from lane half h, which is entries [8u, 8u + 8) of s[kb] and one 16-byte V^T chunk.
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int kc = 2 * kb + u;
-          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(vbase + (16 * kc) * S::kVStride + 32 * db));
-          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (lds_bf16x4*)(vbase + (16 * kc + 8) * S::kVStride + 32 * db));
-          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(v_lds + vt_off[db] + 2 * (16 * kb + 4 * u));
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[u], o[db], 0, 0, 0);
         }
       }
