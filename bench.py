@@ -44,6 +44,28 @@ def parse_args():
     return ap.parse_args()
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_traffic_llama128k.md")
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
+    scaled by the copy-probe factors, or None when the counters were taken on other kernel source
+    or another workload."""
+    import hashlib
+    import re
+
+    if workload_name != "llama128k" or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(TRAFFIC_PROFILE).read(), re.S)
+    if not m:
+        return None
+    block = json.loads(m.group(1))
+    src = os.path.join(ROOT, block["kernel_source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != block["kernel_source_sha256"]:
+        return None
+    return int(block["traffic_bytes"])
+
+
 def geometry_work(w, geo):
     """Algorithmic attention FLOPs and the selection-side bytes from the cluster geometry.
 
@@ -227,7 +249,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(w.name),
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
         },
