@@ -36,6 +36,7 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama128k")
     ap.add_argument("--cluster", type=int, default=0, help="cluster size in sub-chunks (0: the workload's)")
+    ap.add_argument("--sweep", default="", help="comma-separated cluster sizes; one JSON line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
     ap.add_argument("--out-bf16", action="store_true")
@@ -93,10 +94,14 @@ def geometry_work(w, geo):
     }
 
 
-def cpu_baseline(w, data, cs, geo, n_tiles, seed=0):
-    """The fp64 oracle as it stands, on a bounded sample: the whole selection (all clusters) plus
-    attention for `n_tiles` random 32-row tiles; the attention time is scaled to the layer by
-    visible-pair count (the oracle's cost is linear in it)."""
+def cpu_baseline(w, data, cs, geo, n_tiles, n_sel_clusters=32, seed=0):
+    """The fp64 oracle as it stands, timed on a bounded sample of one layer and scaled to the
+    workload: representative keys of the blocks the sampled clusters score (scaled by block
+    count), selection for up to `n_sel_clusters` clusters (all of them when there are no more;
+    else the first, the last and random ones, scaled by anchor rows + candidates, the two terms
+    its cost is linear in), and attention for `n_tiles` random 32-row tiles of the sampled
+    clusters (scaled by visible (row, key) pairs). Every layer has the same geometry, so the
+    layer time is multiplied by the layer count."""
     import numpy as np
     import threadpoolctl
 
@@ -104,37 +109,157 @@ def cpu_baseline(w, data, cs, geo, n_tiles, seed=0):
 
     info = threadpoolctl.threadpool_info()
     cores = max([i.get("num_threads", 1) for i in info] or [1])
-    t0 = time.perf_counter()
-    ref = oracle.prefill(data["q"], data["k_pages"], data["v_pages"], data["block_table"], w.n_tokens,
-                         sub_chunk=w.sub_chunk, block_size=w.block_size, top_k=w.top_k,
-                         sink_tokens=w.sink_tokens, local_window=w.local_window, cluster_start=cs,
-                         with_output=False)
-    t_sel = time.perf_counter() - t0
     rng = np.random.default_rng(seed)
-    B = w.block_size
-    sampled_pairs = 0
+    B, Hkv = w.block_size, w.num_kv_heads
+    G = oracle.geometry(w.n_tokens, w.sub_chunk, B, w.sink_tokens, w.local_window, w.top_k, cs)
+    J = len(G)
+    if J <= n_sel_clusters:
+        sample = list(range(J))
+    else:
+        rest = rng.choice(np.arange(1, J - 1), size=n_sel_clusters - 2, replace=False)
+        sample = sorted({0, J - 1, *rest.tolist()})
+    n_rep = max(G[j].sink_blk + G[j].n_cand for j in sample)
+
+    t0 = time.perf_counter()
+    k_rep = oracle.rep_keys(data["k_pages"], data["block_table"], w.n_tokens, B, blocks=np.arange(n_rep))
+    t_rep = (time.perf_counter() - t0) * (w.n_tokens // B) / max(n_rep, 1)
+
+    sels = {}
     t1 = time.perf_counter()
+    for j in sample:
+        g = G[j]
+        v = oracle.anchor_fingerprint(data["q"], g.s, g.anchor_end)
+        x = oracle.block_logits(v, k_rep[g.sink_blk:g.sink_blk + g.n_cand], Hkv)
+        sels[j], _ = oracle.select_topk(oracle.soft_vote(x), g.sink_blk, w.top_k)
+    cost = [(g.anchor_end - g.s) + g.n_cand for g in G]
+    t_sel = (time.perf_counter() - t1) * sum(cost) / max(sum(cost[j] for j in sample), 1)
+
+    sampled_pairs = 0
+    t2 = time.perf_counter()
     for _ in range(n_tiles):
-        j = int(rng.integers(0, len(ref["geometry"])))
-        g = ref["geometry"][j]
+        j = sample[int(rng.integers(0, len(sample)))]
+        g = G[j]
         p0 = g.s + 32 * int(rng.integers(0, max(1, (g.e - g.s) // 32)))
         rows = np.arange(p0, min(p0 + 32, g.e))
-        oracle.attention_rows(data["q"], data["k_pages"], data["v_pages"], data["block_table"], g,
-                              ref["selections"][j], rows, B)
+        oracle.attention_rows(data["q"], data["k_pages"], data["v_pages"], data["block_table"], g, sels[j], rows, B)
         sampled_pairs += len(rows) * (g.sink_eff + g.sel_cnt) * B + int(sum(p - g.lo_blk * B + 1 for p in rows))
-    t_att = time.perf_counter() - t1
+    t_att_raw = time.perf_counter() - t2
     total_pairs = geometry_work(w, geo)["pairs"]
-    t_layer = t_sel + t_att * total_pairs / max(sampled_pairs, 1)
+    t_layer = t_rep + t_sel + t_att_raw * total_pairs / max(sampled_pairs, 1)
+    measured = time.perf_counter() - t0
     return {
-        "value": w.n_tokens * w.layers / t_layer,
+        "value": w.n_tokens / (t_layer * w.layers),
         "unit": "tokens/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": (f"fp64 numpy oracle: selection for all {len(cs) - 1} clusters ({t_sel:.1f} s) + attention of "
-                   f"{n_tiles} random 32-row tiles x {w.num_q_heads} heads ({t_att:.1f} s), scaled to the layer "
-                   f"by visible (row, key) pairs ({sampled_pairs} of {total_pairs})"),
-        "seconds_measured": round(t_sel + t_att, 2),
+        "sample": (f"fp64 numpy oracle on layer 0: representative keys of {n_rep} of {w.n_tokens // B} blocks, "
+                   f"selection of {len(sample)} of {J} clusters, attention of {n_tiles} random 32-row tiles x "
+                   f"{w.num_q_heads} heads ({sampled_pairs} of {total_pairs} visible (row, key) pairs); each part "
+                   f"scaled to the layer, x{w.layers} layers"),
+        "seconds_measured": round(measured, 2),
     }
+
+
+def time_path(args, w, c, layers, dev):
+    """Times `args.steps` steps of the whole path (every layer) for cluster size c; returns the
+    result dict without the CPU baseline."""
+    import gen
+    import paper_2609_31568_amd as pk
+    import torch
+
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    cfg = pk.config_for(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
+                        block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=w.top_k, sink_tokens=w.sink_tokens,
+                        local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=len(cs) - 1,
+                        out_bf16=args.out_bf16)
+    geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
+    work = geometry_work(w, geo)
+    h = pk.Scale(cfg)
+    # one set of outputs shared by the layers: each layer's output is complete when its attention
+    # call ends, and the next layer's calls are ordered after it on the stream
+    bufs = pk.LayerBuffers(cfg, w.n_tokens, len(cs) - 1, device=dev)
+
+    def step():
+        for q, kp, vp, bt in layers:
+            pk.run_layer(h, q, kp, vp, bt, w.n_tokens, cs, bufs)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    h.enable_timing(True)
+    h.stage_times(reset=True)
+    calls0 = h.retrieval_calls()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = h.stage_times(reset=True)
+    calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
+    h.close()
+    del bufs
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tokens_per_s = w.n_tokens / (ms_per_step / 1e3)
+    per_launch = {k: (ms / n if n else 0.0) for k, (ms, n) in stages.items()}
+    att_ms = per_launch["attention"]
+    achieved = work["attention_flops"] / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
+
+    def gbs(nbytes, ms):
+        return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
+
+    hbm = {
+        "rep_keys": {"GB/s": gbs(work["rep_keys_bytes"], per_launch["rep_keys"]), "bytes": work["rep_keys_bytes"]},
+        "fingerprint": {"GB/s": gbs(work["fingerprint_bytes"], per_launch["fingerprint"]),
+                        "bytes": work["fingerprint_bytes"]},
+        "logits": {"GB/s": gbs(work["logits_bytes"], per_launch["logits"]), "bytes": work["logits_bytes"],
+                   "note": "effective: k_rep bytes counted once per cluster that scores them (the per-call cost "
+                           "model); the kernel reads them from L2 / MALL"},
+        "vote_topk": {"GB/s": gbs(work["vote_bytes"], per_launch["vote_topk"]), "bytes": work["vote_bytes"]},
+        "peak_GB/s": PEAK_HBM_GBS,
+    }
+    shape = ("Llama-3-8B-shaped attention layer" if w.num_q_heads == 32 else "Qwen2-7B-shaped attention stack")
+    return {
+        "metric": METRIC,
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded topic-structured Q/K/V, bf16)",
+        "config": {
+            "workload": f"{w.name}: {w.layers} x {shape}, {w.n_tokens} tokens",
+            "n_tokens": w.n_tokens, "layers": w.layers, "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": w.block_size,
+            "sub_chunk": w.sub_chunk, "cluster": c, "top_k": w.top_k, "sink_tokens": w.sink_tokens,
+            "local_window": w.local_window, "out_dtype": "bf16" if args.out_bf16 else "fp32",
+            "seed": w.seed,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "sparse_attention",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": measured_traffic(w.name) if c == gen.WORKLOADS[w.name].cluster else None,
+            "flops_per_launch": work["attention_flops"],
+            "avg_launch_ms": round(att_ms, 4),
+        },
+        "mfma_util_pct": round(100 * achieved / PEAK_BF16_TFLOPS, 2),
+        "layer_tokens_per_s": round(w.n_tokens * w.layers / (ms_per_step / 1e3), 1),
+        "stage_ms_per_layer": {k: round(v, 4) for k, v in per_launch.items()},
+        "hbm": hbm,
+        "retrieval_calls": {"per_step": int(calls), "per_layer": len(cs) - 1, "clusters": len(cs) - 1,
+                            "per_sub_chunk_baseline": w.n_sub_chunks * w.layers,
+                            "reduction": round(w.n_sub_chunks * w.layers / max(calls, 1), 2)},
+    }, cs, geo
 
 
 def main():
@@ -149,7 +274,6 @@ def main():
     import torch
 
     import gen
-    import paper_2609_31568_amd as pk
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -165,105 +289,32 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": a.numel() * 4, "copy_probe_bytes_written": b.numel() * 4}))
         return
     w = gen.WORKLOADS[args.workload]
-    c = args.cluster or w.cluster
-    w = w.with_(cluster=c)
-    print(f"[bench] generating {w.name}: N={w.n_tokens} Hq={w.num_q_heads} Hkv={w.num_kv_heads} d={w.head_dim} "
-          f"B={w.block_size} L={w.sub_chunk} c={c} k={w.top_k}", file=sys.stderr, flush=True)
-    t_gen = time.perf_counter()
-    data = gen.make_layer(w)
-    cs = gen.cluster_starts(w.n_sub_chunks, c)
-    print(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
+    sweep = [int(x) for x in args.sweep.split(",")] if args.sweep else [args.cluster or w.cluster]
 
     def up(a):
         return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
 
-    q, kp, vp, bt = up(data["q"]), up(data["k_pages"]), up(data["v_pages"]), up(data["block_table"])
-    cfg = pk.config_for(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
-                        block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=w.top_k, sink_tokens=w.sink_tokens,
-                        local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=len(cs) - 1,
-                        out_bf16=args.out_bf16)
-    geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
-    work = geometry_work(w, geo)
-    h = pk.Scale(cfg)
-    bufs = pk.LayerBuffers(cfg, w.n_tokens, len(cs) - 1, device=dev)
+    t_gen = time.perf_counter()
+    layers, host0 = [], None
+    for layer in range(w.layers):
+        print(f"[bench] generating {w.name} layer {layer}: N={w.n_tokens} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
+              f"d={w.head_dim} B={w.block_size} L={w.sub_chunk} k={w.top_k}", file=sys.stderr, flush=True)
+        data = gen.make_layer(w, layer)
+        layers.append((up(data["q"]), up(data["k_pages"]), up(data["v_pages"]), up(data["block_table"])))
+        if layer == 0:
+            host0 = data
+        del data
+    print(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
 
-    for _ in range(args.warmup):
-        pk.run_layer(h, q, kp, vp, bt, w.n_tokens, cs, bufs)
-    torch.cuda.synchronize()
-    h.enable_timing(True)
-    h.stage_times(reset=True)
-    calls0 = h.retrieval_calls()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        pk.run_layer(h, q, kp, vp, bt, w.n_tokens, cs, bufs)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    stages = h.stage_times(reset=True)
-    calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
-    h.close()
-
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    tokens_per_s = w.n_tokens * w.layers / (ms_per_step / 1e3)
-    per_launch = {k: (ms / n if n else 0.0) for k, (ms, n) in stages.items()}
-    att_ms = per_launch["attention"]
-    achieved = work["attention_flops"] / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
-
-    def gbs(nbytes, ms):
-        return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
-
-    hbm = {
-        "rep_keys": {"GB/s": gbs(work["rep_keys_bytes"], per_launch["rep_keys"]), "bytes": work["rep_keys_bytes"]},
-        "fingerprint": {"GB/s": gbs(work["fingerprint_bytes"], per_launch["fingerprint"]),
-                        "bytes": work["fingerprint_bytes"]},
-        "logits": {"GB/s": gbs(work["logits_bytes"], per_launch["logits"]), "bytes": work["logits_bytes"],
-                   "note": "k_rep re-read per cluster; largely L2/MALL resident at this size"},
-        "vote_topk": {"GB/s": gbs(work["vote_bytes"], per_launch["vote_topk"]), "bytes": work["vote_bytes"]},
-        "peak_GB/s": PEAK_HBM_GBS,
-    }
-    result = {
-        "metric": METRIC,
-        "value": round(tokens_per_s, 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded topic-structured Q/K/V, bf16)",
-        "config": {
-            "workload": f"{w.name}: one Llama-3-8B-shaped attention layer, {w.n_tokens} tokens",
-            "n_tokens": w.n_tokens, "layers": w.layers, "num_q_heads": w.num_q_heads,
-            "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": w.block_size,
-            "sub_chunk": w.sub_chunk, "cluster": c, "top_k": w.top_k, "sink_tokens": w.sink_tokens,
-            "local_window": w.local_window, "out_dtype": "bf16" if args.out_bf16 else "fp32",
-            "seed": w.seed,
-        },
-        "roofline": {
-            "bound": "mfma",
-            "kernel": "sparse_attention",
-            "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(w.name),
-            "flops_per_launch": work["attention_flops"],
-            "avg_launch_ms": round(att_ms, 4),
-        },
-        "mfma_util_pct": round(100 * achieved / PEAK_BF16_TFLOPS, 2),
-        "stage_ms_per_step": {k: round(v, 4) for k, v in per_launch.items()},
-        "hbm": hbm,
-        "retrieval_calls": {"per_step": int(calls), "clusters": len(cs) - 1, "per_sub_chunk_baseline": w.n_sub_chunks,
-                            "reduction": round(w.n_sub_chunks / max(calls, 1), 2)},
-    }
-    if rank == 0 and not args.no_cpu_baseline:
-        print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(w, data, cs, geo, args.cpu_tiles)
-    if rank == 0:
-        print(json.dumps(result), flush=True)
+    for c in sweep:
+        wc = w.with_(cluster=c)
+        print(f"[bench] timing c={c}", file=sys.stderr, flush=True)
+        result, cs, geo = time_path(args, wc, c, layers, dev)
+        if rank == 0 and not args.no_cpu_baseline:
+            print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
+            result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles)
+        if rank == 0:
+            print(json.dumps(result), flush=True)
 
 
 if __name__ == "__main__":

@@ -75,7 +75,7 @@ typedef struct {
   int32_t head_dim;      /* d: 64 or 128                                                     */
   int32_t block_size;    /* B: 64 or 128 tokens per KV block / page                          */
   int32_t sub_chunk;     /* L: query rows per sub-chunk, a positive multiple of B            */
-  int32_t top_k;         /* k >= 0 blocks selected per cluster (at most 64)                  */
+  int32_t top_k;         /* k >= 0 blocks selected per cluster (any size; sel_idx rows hold k) */
   int32_t sink_tokens;   /* S >= 0: attention-sink tokens, rounded up to whole blocks        */
   int32_t local_window;  /* W >= 0: base local window in tokens                              */
   int32_t max_tokens;    /* capacity: largest n_tokens any call will pass (sizes scratch)    */

@@ -35,23 +35,27 @@ hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, 
                            int num_kv_heads, int block_size, int head_dim, float* k_rep,
                            hipStream_t stream);
 
-// Anchor fingerprints: partial fp64 row sums per (cluster, row chunk), then fp32 means.
-// `partial` holds n_clusters * fp_chunks * Hq * d doubles.
+// Anchor fingerprints: fp32 mean of each cluster's anchor rows (fp64 sums).
 hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
-                               int num_q_heads, int head_dim, int sub_chunk, int fp_chunks,
-                               double* partial, float* fingerprints, hipStream_t stream);
+                               int num_q_heads, int head_dim, float* fingerprints, hipStream_t stream);
 
-// Selection logits x[j][h][c] for candidate c of cluster j (row stride `cand_stride`).
+// Candidate chunks of the selection kernels for `max_cand` candidates; head_stats holds
+// n_clusters * Hq * selection_chunks(max_cand) (max, sum) pairs.
+int selection_chunks(int max_cand);
+
+// Selection logits x[j][h][c] for candidate c of cluster j (row stride `cand_stride`), and each
+// candidate chunk's softmax partials per head.
 hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
                                int n_clusters, int max_cand, int cand_stride, int sink_blk,
                                int num_q_heads, int num_kv_heads, int head_dim, float score_scale,
-                               float* logits, hipStream_t stream);
+                               float* logits, float2* head_stats, hipStream_t stream);
 
 // Soft-voting scores and deterministic top-k per cluster.
-hipError_t launch_vote_topk(const float* logits, const ClusterGeo* geo, int n_clusters,
-                            int cand_stride, int sink_blk, int num_q_heads, int top_k,
-                            int n_blocks, float* scores_lds_spill, int32_t* sel_idx,
-                            int32_t* sel_cnt, float* scores_out, hipStream_t stream);
+hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo,
+                            int n_clusters, int max_cand, int cand_stride, int sink_blk,
+                            int num_q_heads, int top_k, int n_blocks, float* spill,
+                            int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                            hipStream_t stream);
 
 // Block-sparse attention over the work list.
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
@@ -60,9 +64,6 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
                                    const int32_t* sel_cnt, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, hipStream_t stream);
-
-// Row chunks of fingerprint_partial for a sub-chunk of `sub_chunk` rows.
-int fingerprint_chunks(int sub_chunk);
 
 // Query positions per attention work item for a group of `group` query heads per KV head
 // (a multiple of kTilePositions), and the number of head groups one KV head's query heads are

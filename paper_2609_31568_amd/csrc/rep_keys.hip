@@ -13,26 +13,31 @@ namespace {
 
 constexpr int kThreads = 256;
 
-template <int D>
+template <int D, int B>
 __global__ __launch_bounds__(kThreads) void rep_keys_kernel(const uint16_t* __restrict__ k_pages,
                                                             const int32_t* __restrict__ block_table,
-                                                            int num_kv_heads, int block_size,
-                                                            float* __restrict__ k_rep) {
+                                                            int num_kv_heads, float* __restrict__ k_rep) {
   constexpr int kChunks = D / 8;                 // 16-byte chunks per row
   constexpr int kRowGroups = kThreads / kChunks; // rows handled in parallel
+  constexpr int kRowsPerThread = B / kRowGroups; // all of a thread's loads are issued together
+  static_assert(B % kRowGroups == 0, "whole rows per thread");
   const int b = blockIdx.x / num_kv_heads;
   const int g = blockIdx.x % num_kv_heads;
   const int page = block_table ? block_table[b] : b;
-  const uint16_t* tile = k_pages + ((int64_t)page * num_kv_heads + g) * block_size * D;
+  const uint16_t* tile = k_pages + ((int64_t)page * num_kv_heads + g) * B * D;
 
   const int chunk = threadIdx.x % kChunks;
   const int rg = threadIdx.x / kChunks;
   double acc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.0;
-  for (int r = rg; r < block_size; r += kRowGroups) {
-    const uint4 v = *reinterpret_cast<const uint4*>(tile + (int64_t)r * D + chunk * 8);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  uint4 v[kRowsPerThread];
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u)
+    v[u] = *reinterpret_cast<const uint4*>(tile + (int64_t)(rg + u * kRowGroups) * D + chunk * 8);
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u) {
+    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       acc[2 * i] += (double)__uint_as_float(w[i] << 16);
@@ -47,7 +52,7 @@ __global__ __launch_bounds__(kThreads) void rep_keys_kernel(const uint16_t* __re
     double s = 0.0;
 #pragma unroll 4
     for (int r = 0; r < kRowGroups; ++r) s += part[r][threadIdx.x];
-    k_rep[((int64_t)b * num_kv_heads + g) * D + threadIdx.x] = (float)(s / (double)block_size);
+    k_rep[((int64_t)b * num_kv_heads + g) * D + threadIdx.x] = (float)(s / (double)B);
   }
 }
 
@@ -58,10 +63,14 @@ hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, 
                            hipStream_t stream) {
   if (n_blocks <= 0) return hipSuccess;
   const dim3 grid((unsigned)((int64_t)n_blocks * num_kv_heads));
-  if (head_dim == 128)
-    rep_keys_kernel<128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, block_size, k_rep);
+  if (head_dim == 128 && block_size == 128)
+    rep_keys_kernel<128, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+  else if (head_dim == 128)
+    rep_keys_kernel<128, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+  else if (block_size == 128)
+    rep_keys_kernel<64, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
   else
-    rep_keys_kernel<64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, block_size, k_rep);
+    rep_keys_kernel<64, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
   return hipGetLastError();
 }
 

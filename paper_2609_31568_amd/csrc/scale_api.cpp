@@ -43,12 +43,11 @@ struct scale_ctx {
   int device = 0;
   int64_t retrieval_calls = 0;
   int max_blocks = 0;        // max_tokens / B (rounded up)
-  int fp_chunks = 0;
   int max_items = 0;
   // device scratch
   ClusterGeo* d_geo = nullptr;
   WorkItem* d_items = nullptr;
-  double* d_fp_partial = nullptr;
+  float2* d_head_stats = nullptr;
   float* d_fingerprints = nullptr;
   float* d_logits = nullptr;
   float* d_spill = nullptr;
@@ -160,7 +159,7 @@ void release(scale_ctx* h) {
   }
   (void)hipFree(h->d_geo);
   (void)hipFree(h->d_items);
-  (void)hipFree(h->d_fp_partial);
+  (void)hipFree(h->d_head_stats);
   (void)hipFree(h->d_fingerprints);
   (void)hipFree(h->d_logits);
   (void)hipFree(h->d_spill);
@@ -236,7 +235,6 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
   if (hipGetDevice(&h->device) != hipSuccess) { release(h); return SCALE_ERR_HIP; }
   const scale_config& c = h->cfg;
   h->max_blocks = (c.max_tokens + c.block_size - 1) / c.block_size;
-  h->fp_chunks = scale::fingerprint_chunks(c.sub_chunk);
   h->max_items = (int)max_work_items(c);
   const int64_t row_elems = (int64_t)c.num_q_heads * c.head_dim;
   const int64_t mc = c.max_clusters;
@@ -247,7 +245,7 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
   };
   bool ok = dev((void**)&h->d_geo, sizeof(ClusterGeo) * mc) &&
             dev((void**)&h->d_items, sizeof(WorkItem) * (size_t)h->max_items) &&
-            dev((void**)&h->d_fp_partial, sizeof(double) * mc * h->fp_chunks * row_elems) &&
+            dev((void**)&h->d_head_stats, sizeof(float2) * mc * c.num_q_heads * scale::selection_chunks(h->max_blocks)) &&
             dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
             dev((void**)&h->d_logits, sizeof(float) * mc * c.num_q_heads * (int64_t)h->max_blocks) &&
             dev((void**)&h->d_spill, h->max_blocks > 8192 ? sizeof(float) * mc * h->max_blocks : 0);
@@ -315,18 +313,17 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
   const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
   float* fps = fingerprints_out ? fingerprints_out : h->d_fingerprints;
   stage_begin(h);
-  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, c.sub_chunk,
-                                               h->fp_chunks, h->d_fp_partial, fps, h->stream));
+  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, h->stream));
   stage_end(h, SCALE_STAGE_FINGERPRINT);
   if (st != SCALE_OK) return st;
   stage_begin(h);
   st = check_launch(scale::launch_block_logits(fps, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
                                                c.num_q_heads, c.num_kv_heads, c.head_dim, sigma, h->d_logits,
-                                               h->stream));
+                                               h->d_head_stats, h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
   stage_begin(h);
-  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_geo, n_clusters, h->max_blocks, sink_blk,
+  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_head_stats, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
                                             c.num_q_heads, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
                                             scores_out, h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);

@@ -2,15 +2,18 @@
 // deterministic top-k, once per cluster (paper Sec. 5.1.3, Eq. 9 and the head soft-voting
 // instantiation of the selection function).
 //
-//  fingerprint_partial  (cluster, row chunk) -> fp64 column sums of the anchor rows, all heads
-//  fingerprint_final    cluster -> fp32 mean = fixed-order sum of the partials / anchor length
-//  block_logits         (cluster, candidate chunk) -> x[h][c] = sigma * v[h] . k_rep[c][g(h)]
-//  vote_topk            cluster -> per-head softmax over candidates, sum over heads, top-k by
-//                       (score desc, block index asc), emitted ascending
+//  fingerprint   (column slice, cluster) -> fp32 mean of the anchor rows (fp64 sums)
+//  block_logits  (cluster, candidate chunks, KV head) -> x[h][c] = sigma * v[h] . k_rep[c][g(h)]
+//                for the query heads h of KV head g, plus each chunk's softmax partials
+//                (max_c x[h][c], sum_c exp(x[h][c] - max)) per head
+//  vote_topk     cluster -> per-head softmax normaliser from the chunk partials, score = sum over
+//                heads of the softmax weights, top-k by (score desc, block index asc), ascending
 //
 // All of it is HBM/L2-bandwidth work (a few FLOP per byte); every reduction has a fixed order,
 // so two runs give identical bits.
 #include <float.h>
+
+#include <algorithm>
 
 #include "common.h"
 
@@ -18,124 +21,156 @@ namespace scale {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kFpRowsPerChunk = 64;   // anchor rows per fingerprint_partial work-group
+constexpr int kFpThreads = 512;          // fingerprint: 8 waves
+constexpr int kFpCols = 512;             // columns of the Hq*d row per fingerprint work-group
+constexpr int kFpRowsInFlight = 4;       // 16-byte loads in flight per lane
+constexpr int kCandChunk = 64;           // candidates per block_logits step
+constexpr int kLogitsTargetGroups = 4096;
 
-// grid: (row chunk, cluster); each thread owns 8 consecutive columns of the Hq*d row.
-__global__ __launch_bounds__(kThreads) void fingerprint_partial(const uint16_t* __restrict__ q,
-                                                                const ClusterGeo* __restrict__ geo,
-                                                                int row_elems, int fp_chunks,
-                                                                double* __restrict__ partial) {
+// grid: (column slice, cluster). Lane l of wave w owns the 8 columns [slice*512 + 8l, +8) and
+// sums anchor rows w, w+8, w+16, ... in fp64 (exact for bf16 inputs of moderate range); the 8
+// waves' sums are combined in LDS in wave order and divided once.
+__global__ __launch_bounds__(kFpThreads) void fingerprint_kernel(const uint16_t* __restrict__ q,
+                                                                 const ClusterGeo* __restrict__ geo,
+                                                                 int row_elems, float* __restrict__ fingerprints) {
+  constexpr int kWaves = kFpThreads / 64;
+  __shared__ double part[kWaves][kFpCols];
   const int j = blockIdx.y;
-  const int chunk = blockIdx.x;
   const ClusterGeo G = geo[j];
-  const int r0 = G.s + chunk * kFpRowsPerChunk;
-  const int r1 = min(G.anchor_end, r0 + kFpRowsPerChunk);
-  double* dst = partial + ((int64_t)j * fp_chunks + chunk) * row_elems;
-  for (int c0 = threadIdx.x * 8; c0 < row_elems; c0 += kThreads * 8) {
-    double acc[8];
+  const int n_rows = G.anchor_end - G.s;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int col = blockIdx.x * kFpCols + lane * 8;
+  double acc[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = 0.0;
-    for (int r = r0; r < r1; ++r) {
-      const uint4 v = *reinterpret_cast<const uint4*>(q + (int64_t)r * row_elems + c0);
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0;
+  if (col < row_elems) {   // row_elems is a multiple of 64, so a lane's 8 columns are all in range
+    const uint16_t* base = q + (int64_t)G.s * row_elems + col;
+    auto add = [&](const uint4& v) {
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         acc[2 * i] += (double)__uint_as_float(w[i] << 16);
         acc[2 * i + 1] += (double)__uint_as_float(w[i] & 0xFFFF0000u);
       }
-    }
+    };
+    int r = wave;
+    for (; r + (kFpRowsInFlight - 1) * kWaves < n_rows; r += kFpRowsInFlight * kWaves) {
+      uint4 v[kFpRowsInFlight];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) dst[c0 + i] = acc[i];
+      for (int u = 0; u < kFpRowsInFlight; ++u)
+        v[u] = *reinterpret_cast<const uint4*>(base + (int64_t)(r + u * kWaves) * row_elems);
+#pragma unroll
+      for (int u = 0; u < kFpRowsInFlight; ++u) add(v[u]);
+    }
+    for (; r < n_rows; r += kWaves) add(*reinterpret_cast<const uint4*>(base + (int64_t)r * row_elems));
   }
-}
-
-// grid: cluster; sums the partials of its chunks in chunk order.
-__global__ __launch_bounds__(kThreads) void fingerprint_final(const double* __restrict__ partial,
-                                                              const ClusterGeo* __restrict__ geo,
-                                                              int row_elems, int fp_chunks,
-                                                              float* __restrict__ fingerprints) {
-  const int j = blockIdx.x;
-  const ClusterGeo G = geo[j];
-  const int n_rows = G.anchor_end - G.s;
-  const int used = (n_rows + kFpRowsPerChunk - 1) / kFpRowsPerChunk;
-  const double* src = partial + (int64_t)j * fp_chunks * row_elems;
-  for (int c = threadIdx.x; c < row_elems; c += kThreads) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) part[wave][lane * 8 + i] = acc[i];
+  __syncthreads();
+  const int c = blockIdx.x * kFpCols + threadIdx.x;
+  if (threadIdx.x < kFpCols && c < row_elems) {
     double s = 0.0;
-    for (int k = 0; k < used; ++k) s += src[(int64_t)k * row_elems + c];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += part[w][threadIdx.x];
     fingerprints[(int64_t)j * row_elems + c] = (float)(s / (double)n_rows);
   }
 }
 
-// grid: (candidate chunk of 64, cluster). Thread t of the work-group owns candidate
-// (chunk * 64 + t % 64) and the KV heads g = t / 64, t / 64 + 4, ...; it forms the dot products
-// of k_rep[b][g] with the fingerprints of the query heads reading KV head g.
+// grid: linear over (cluster j, part p, KV head g) with g fastest: work-groups are handed to the
+// 8 XCDs round-robin, so one XCD reads one KV head's slice of k_rep from its own L2. The work-group
+// takes candidate chunks p, p + parts, ... of cluster j. In a chunk, wave w holds candidates
+// [16w, 16w + 16) with four lanes per candidate; lane quarter q loads the float4s {4i + q} of the
+// candidate's representative key (64 contiguous bytes per candidate per load), forms partial dot
+// products with the fingerprints of the (at most 8) query heads of g held in LDS, and the four
+// lanes add their partials.
 template <int D>
 __global__ __launch_bounds__(kThreads) void block_logits_kernel(
     const float* __restrict__ fingerprints, const float* __restrict__ k_rep,
-    const ClusterGeo* __restrict__ geo, int cand_stride, int sink_blk, int num_q_heads,
-    int num_kv_heads, float score_scale, float* __restrict__ logits) {
-  extern __shared__ float v_lds[];                  // [Hq][D] fingerprints of this cluster
-  const int j = blockIdx.y;
+    const ClusterGeo* __restrict__ geo, int parts, int n_chunks, int cand_stride, int sink_blk,
+    int num_q_heads, int num_kv_heads, float score_scale, float* __restrict__ logits,
+    float2* __restrict__ head_stats) {
+  constexpr int kVec = D / 16;                      // float4 loads per lane
+  __shared__ float4 v_lds[8 * D / 4];               // fingerprints of the query heads of g
+  __shared__ float red[kThreads / 64][8];
+  const int g = blockIdx.x % num_kv_heads;
+  const int rest = blockIdx.x / num_kv_heads;
+  const int p = rest % parts;
+  const int j = rest / parts;
   const ClusterGeo G = geo[j];
-  const int c = blockIdx.x * 64 + threadIdx.x % 64;
-  if (blockIdx.x * 64 >= G.n_cand) return;          // uniform over the work-group
-  const int row_elems = num_q_heads * D;
-  for (int i = threadIdx.x; i < row_elems; i += kThreads) v_lds[i] = fingerprints[(int64_t)j * row_elems + i];
+  const int chunks = (G.n_cand + kCandChunk - 1) / kCandChunk;
+  if (p >= chunks) return;                          // uniform over the work-group
+  const int group = num_q_heads / num_kv_heads;     // <= 8
+  const float4* vsrc = reinterpret_cast<const float4*>(fingerprints + ((int64_t)j * num_q_heads + g * group) * D);
+  for (int i = threadIdx.x; i < group * D / 4; i += kThreads) v_lds[i] = vsrc[i];
   __syncthreads();
-  if (c >= G.n_cand) return;
-  const int group = num_q_heads / num_kv_heads;
-  const int b = sink_blk + c;
-  for (int g = threadIdx.x / 64; g < num_kv_heads; g += kThreads / 64) {
-    const float4* kr = reinterpret_cast<const float4*>(k_rep + ((int64_t)b * num_kv_heads + g) * D);
-    for (int h0 = 0; h0 < group; h0 += 4) {
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
-      const int nh = min(4, group - h0);
-      for (int i = 0; i < D / 4; ++i) {
-        const float4 k4 = kr[i];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int q4 = lane & 3;
+  for (int chunk = p; chunk < chunks; chunk += parts) {
+    const int c = chunk * kCandChunk + wave * 16 + lane / 4;
+    const bool valid = c < G.n_cand;
+    float4 kv[kVec];
+    const float4* kr = reinterpret_cast<const float4*>(k_rep + ((int64_t)(sink_blk + (valid ? c : 0)) * num_kv_heads + g) * D);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (u < nh) {
-            const float* v = v_lds + (g * group + h0 + u) * D + 4 * i;
-            acc[u] = fmaf(v[0], k4.x, acc[u]);
-            acc[u] = fmaf(v[1], k4.y, acc[u]);
-            acc[u] = fmaf(v[2], k4.z, acc[u]);
-            acc[u] = fmaf(v[3], k4.w, acc[u]);
-          }
+    for (int i = 0; i < kVec; ++i) kv[i] = kr[4 * i + q4];
+    float x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      x[u] = 0.f;
+      if (u < group) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) {
+          const float4 v = v_lds[u * (D / 4) + 4 * i + q4];
+          acc = fmaf(v.x, kv[i].x, acc);
+          acc = fmaf(v.y, kv[i].y, acc);
+          acc = fmaf(v.z, kv[i].z, acc);
+          acc = fmaf(v.w, kv[i].w, acc);
         }
+        acc += __shfl_xor(acc, 1, 64);
+        acc += __shfl_xor(acc, 2, 64);
+        x[u] = score_scale * acc;
+        if (valid && q4 == (u & 3))
+          logits[((int64_t)j * num_q_heads + g * group + u) * cand_stride + c] = x[u];
       }
-      for (int u = 0; u < nh; ++u)
-        logits[((int64_t)j * num_q_heads + g * group + h0 + u) * cand_stride + c] = score_scale * acc[u];
     }
+    // softmax partials of this chunk per head: max over its candidates, then sum of exp(x - max)
+    float m[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      float t = valid ? x[u] : -FLT_MAX;
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1) t = fmaxf(t, __shfl_xor(t, o, 64));
+      m[u] = t;
+    }
+    if (lane == 0)
+      for (int u = 0; u < group; ++u) red[wave][u] = m[u];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) m[u] = fmaxf(fmaxf(red[0][u], red[1][u]), fmaxf(red[2][u], red[3][u]));
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      float t = (valid && u < group) ? expf(x[u] - m[u]) : 0.f;
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1) t += __shfl_xor(t, o, 64);
+      if (lane == 0 && u < group) red[wave][u] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x < group) {
+      const int u = threadIdx.x;
+      const float s = (red[0][u] + red[1][u]) + (red[2][u] + red[3][u]);
+      head_stats[((int64_t)j * num_q_heads + g * group + u) * n_chunks + chunk] = make_float2(m[u], s);
+    }
+    __syncthreads();
   }
 }
 
-// ---- block-wide helpers with a fixed reduction order ----
-__device__ inline float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-// Block-wide reductions for kThreads = 256 (4 waves); `red` holds 4 floats / ints.
-__device__ inline float block_max(float v, float* red) {
-  v = wave_max(v);
-  __syncthreads();
-  if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = v;
-  __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
-__device__ inline float block_sum(float v, float* red) {
-  v = wave_sum(v);
-  __syncthreads();
-  if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = v;
-  __syncthreads();
-  return (red[0] + red[1]) + (red[2] + red[3]);
-}
-// Exclusive prefix sum over threads in thread order; returns the total through *total.
+// ---- vote_topk ----
+constexpr int kVoteThreads = 1024;
+constexpr int kVoteWaves = kVoteThreads / 64;
+constexpr int kMaxLdsCand = 8192;        // scores of larger clusters live in the global spill row
+
+// Exclusive prefix sum over the work-group's threads in thread order; the total through *total.
 __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
   const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
   int incl = v;
@@ -147,23 +182,34 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
   __syncthreads();
   if (lane == 63) red[wave] = incl;
   __syncthreads();
-  int before = 0;
-  for (int w = 0; w < wave; ++w) before += red[w];
-  *total = red[0] + red[1] + red[2] + red[3];
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kVoteWaves; ++w) {
+    before += w < wave ? red[w] : 0;
+    all += red[w];
+  }
+  *total = all;
   return before + incl - v;
 }
 
-// grid: cluster. Scores live in LDS when n_cand fits, else in `spill` (global, per cluster).
-constexpr int kMaxLdsCand = 8192;
-
-__global__ __launch_bounds__(kThreads) void vote_topk_kernel(
-    const float* __restrict__ logits, const ClusterGeo* __restrict__ geo, int cand_stride,
-    int sink_blk, int num_q_heads, int top_k, int n_blocks, float* __restrict__ spill,
-    int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_cnt, float* __restrict__ scores_out) {
+// grid: cluster.
+//  1. soft-voting: each head's softmax maximum and normaliser over all candidates, combined from
+//     the chunk partials in chunk order; then per candidate the sum over heads, in head order.
+//  2. threshold: the sel_cnt-th largest score, by radix selection on the score bits, 8 bits a
+//     pass from the top (scores are >= 0, so their bit patterns order like their values); the
+//     digit is found with a prefix sum over the 256-bin histogram in descending digit order.
+//  3. selected = score above the threshold, or equal to it and among the first ties in index
+//     order; written in ascending block order by an ordered compaction.
+__global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(
+    const float* __restrict__ logits, const float2* __restrict__ head_stats, const ClusterGeo* __restrict__ geo,
+    int n_chunks, int cand_stride, int sink_blk, int num_q_heads, int top_k, int n_blocks,
+    float* __restrict__ spill, int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_cnt,
+    float* __restrict__ scores_out) {
   __shared__ float score_lds[kMaxLdsCand];
-  __shared__ float red_f[4];
-  __shared__ int red_i[4];
+  __shared__ int red_i[kVoteWaves];
   __shared__ unsigned hist[256];
+  __shared__ int pick[2];
+  extern __shared__ float head_lds[];               // [Hq] maxima, then [Hq] 1 / normaliser
   const int j = blockIdx.x;
   const ClusterGeo G = geo[j];
   const int n = G.n_cand;
@@ -171,23 +217,36 @@ __global__ __launch_bounds__(kThreads) void vote_topk_kernel(
   float* score = n <= kMaxLdsCand ? score_lds : spill + (int64_t)j * cand_stride;
   const float* x = logits + (int64_t)j * num_q_heads * cand_stride;
 
-  // 1. soft-voting: per-head max and normaliser, then the sum over heads, head order fixed.
-  for (int c = threadIdx.x; c < n; c += kThreads) score[c] = 0.f;
-  for (int h = 0; h < num_q_heads; ++h) {
-    const float* xh = x + (int64_t)h * cand_stride;
+  // 1.
+  const int used = (n + kCandChunk - 1) / kCandChunk;
+  for (int h = threadIdx.x; h < num_q_heads; h += kVoteThreads) {
+    const float2* st = head_stats + ((int64_t)j * num_q_heads + h) * n_chunks;
     float m = -FLT_MAX;
-    for (int c = threadIdx.x; c < n; c += kThreads) m = fmaxf(m, xh[c]);
-    m = block_max(m, red_f);
+    for (int k = 0; k < used; ++k) m = fmaxf(m, st[k].x);
     float s = 0.f;
-    for (int c = threadIdx.x; c < n; c += kThreads) s += expf(xh[c] - m);
-    s = block_sum(s, red_f);
-    const float inv = 1.0f / s;
-    for (int c = threadIdx.x; c < n; c += kThreads) score[c] += expf(xh[c] - m) * inv;
+    for (int k = 0; k < used; ++k) s += st[k].y * expf(st[k].x - m);
+    head_lds[h] = m;
+    head_lds[num_q_heads + h] = 1.0f / s;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < n; c += kVoteThreads) {
+    float acc = 0.f;
+    int h = 0;
+    for (; h + 16 <= num_q_heads; h += 16) {
+      float xv[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) xv[u] = x[(int64_t)(h + u) * cand_stride + c];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) acc += expf(xv[u] - head_lds[h + u]) * head_lds[num_q_heads + h + u];
+    }
+    for (; h < num_q_heads; ++h)
+      acc += expf(x[(int64_t)h * cand_stride + c] - head_lds[h]) * head_lds[num_q_heads + h];
+    score[c] = acc;
   }
   __syncthreads();
   if (scores_out) {
     float* so = scores_out + (int64_t)j * n_blocks;
-    for (int b = threadIdx.x; b < n_blocks; b += kThreads) {
+    for (int b = threadIdx.x; b < n_blocks; b += kVoteThreads) {
       const int c = b - sink_blk;
       so[b] = (c >= 0 && c < n) ? score[c] : -1.0f;
     }
@@ -195,37 +254,36 @@ __global__ __launch_bounds__(kThreads) void vote_topk_kernel(
   int32_t* out = sel_idx + (int64_t)j * top_k;
   if (threadIdx.x == 0) sel_cnt[j] = cnt;
 
-  // 2. threshold: the cnt-th largest score (scores are >= 0, so their bit patterns order like
-  //    their values). Radix select, 8 bits per pass, most significant first.
+  // 2.
   unsigned prefix = 0, prefix_mask = 0;
   int want = cnt;             // rank (1-based) of the threshold among the still-matching values
   if (cnt > 0 && cnt < n) {
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = threadIdx.x; i < 256; i += kThreads) hist[i] = 0;
+      if (threadIdx.x < 256) hist[threadIdx.x] = 0;
       __syncthreads();
-      for (int c = threadIdx.x; c < n; c += kThreads) {
+      for (int c = threadIdx.x; c < n; c += kVoteThreads) {
         const unsigned u = __float_as_uint(score[c]);
         if ((u & prefix_mask) == prefix) atomicAdd(&hist[(u >> shift) & 0xFF], 1u);
       }
       __syncthreads();
-      // walk the digits from the top; every thread does the same 256-step walk
-      int acc = 0, digit = 0;
-      for (int dgt = 255; dgt >= 0; --dgt) {
-        const int hcount = (int)hist[dgt];
-        if (acc + hcount >= want) { digit = dgt; break; }
-        acc += hcount;
+      const int h_cnt = threadIdx.x < 256 ? (int)hist[255 - threadIdx.x] : 0;
+      int total = 0;
+      const int above = block_exclusive_scan(h_cnt, red_i, &total);   // values with a larger digit
+      if (threadIdx.x < 256 && above < want && above + h_cnt >= want) {
+        pick[0] = 255 - threadIdx.x;
+        pick[1] = above;
       }
-      want -= acc;
-      prefix |= (unsigned)digit << shift;
+      __syncthreads();
+      want -= pick[1];
+      prefix |= (unsigned)pick[0] << shift;
       prefix_mask |= 0xFFu << shift;
       __syncthreads();
     }
   }
   const unsigned thr = prefix;   // bit pattern of the threshold value (valid when 0 < cnt < n)
 
-  // 3. selected = (score > thr) or (score == thr and among the first `want` ties in index order).
-  //    Thread t owns a contiguous index range, so prefix sums follow index order.
-  const int per = (n + kThreads - 1) / kThreads;
+  // 3. thread t owns a contiguous index range, so prefix sums follow index order.
+  const int per = (n + kVoteThreads - 1) / kVoteThreads;
   const int c0 = min(n, threadIdx.x * per), c1 = min(n, c0 + per);
   int n_tie = 0, n_sel_local = 0;
   if (cnt >= n) {
@@ -258,47 +316,52 @@ __global__ __launch_bounds__(kThreads) void vote_topk_kernel(
       if (take) out[pos++] = sink_blk + c;
     }
   }
-  for (int i = cnt + threadIdx.x; i < top_k; i += kThreads) out[i] = -1;
+  for (int i = cnt + threadIdx.x; i < top_k; i += kVoteThreads) out[i] = -1;
 }
 
 }  // namespace
 
 hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
-                               int num_q_heads, int head_dim, int sub_chunk, int fp_chunks,
-                               double* partial, float* fingerprints, hipStream_t stream) {
+                               int num_q_heads, int head_dim, float* fingerprints, hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
-  (void)sub_chunk;
   const int row_elems = num_q_heads * head_dim;
-  fingerprint_partial<<<dim3(fp_chunks, n_clusters), kThreads, 0, stream>>>(q, geo, row_elems, fp_chunks,
-                                                                            partial);
-  fingerprint_final<<<n_clusters, kThreads, 0, stream>>>(partial, geo, row_elems, fp_chunks, fingerprints);
+  const dim3 grid((row_elems + kFpCols - 1) / kFpCols, n_clusters);
+  fingerprint_kernel<<<grid, kFpThreads, 0, stream>>>(q, geo, row_elems, fingerprints);
   return hipGetLastError();
 }
 
-int fingerprint_chunks(int sub_chunk) { return (sub_chunk + kFpRowsPerChunk - 1) / kFpRowsPerChunk; }
+int selection_chunks(int max_cand) { return (max_cand + kCandChunk - 1) / kCandChunk; }
 
 hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
                                int n_clusters, int max_cand, int cand_stride, int sink_blk,
                                int num_q_heads, int num_kv_heads, int head_dim, float score_scale,
-                               float* logits, hipStream_t stream) {
+                               float* logits, float2* head_stats, hipStream_t stream) {
   if (n_clusters <= 0 || max_cand <= 0) return hipSuccess;
-  const dim3 grid((max_cand + 63) / 64, n_clusters);
-  const size_t lds = (size_t)num_q_heads * head_dim * sizeof(float);
+  const int n_chunks = selection_chunks(max_cand);
+  // enough work-groups to fill the chip, without launching many that find no chunk
+  const int64_t base = (int64_t)n_clusters * num_kv_heads;
+  const int parts = (int)std::min<int64_t>(n_chunks, std::max<int64_t>(1, (kLogitsTargetGroups + base - 1) / base));
+  const dim3 grid((unsigned)(base * parts));
   if (head_dim == 128)
-    block_logits_kernel<128><<<grid, kThreads, lds, stream>>>(fingerprints, k_rep, geo, cand_stride, sink_blk,
-                                                             num_q_heads, num_kv_heads, score_scale, logits);
+    block_logits_kernel<128><<<grid, kThreads, 0, stream>>>(fingerprints, k_rep, geo, parts, n_chunks, cand_stride,
+                                                           sink_blk, num_q_heads, num_kv_heads, score_scale, logits,
+                                                           head_stats);
   else
-    block_logits_kernel<64><<<grid, kThreads, lds, stream>>>(fingerprints, k_rep, geo, cand_stride, sink_blk,
-                                                            num_q_heads, num_kv_heads, score_scale, logits);
+    block_logits_kernel<64><<<grid, kThreads, 0, stream>>>(fingerprints, k_rep, geo, parts, n_chunks, cand_stride,
+                                                          sink_blk, num_q_heads, num_kv_heads, score_scale, logits,
+                                                          head_stats);
   return hipGetLastError();
 }
 
-hipError_t launch_vote_topk(const float* logits, const ClusterGeo* geo, int n_clusters, int cand_stride,
-                            int sink_blk, int num_q_heads, int top_k, int n_blocks, float* spill,
-                            int32_t* sel_idx, int32_t* sel_cnt, float* scores_out, hipStream_t stream) {
+hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo, int n_clusters,
+                            int max_cand, int cand_stride, int sink_blk, int num_q_heads, int top_k, int n_blocks,
+                            float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                            hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
-  vote_topk_kernel<<<n_clusters, kThreads, 0, stream>>>(logits, geo, cand_stride, sink_blk, num_q_heads, top_k,
-                                                        n_blocks, spill, sel_idx, sel_cnt, scores_out);
+  const size_t lds = sizeof(float) * 2 * (size_t)num_q_heads;
+  vote_topk_kernel<<<n_clusters, kVoteThreads, lds, stream>>>(logits, head_stats, geo, selection_chunks(max_cand),
+                                                          cand_stride, sink_blk, num_q_heads, top_k, n_blocks, spill,
+                                                          sel_idx, sel_cnt, scores_out);
   return hipGetLastError();
 }
 

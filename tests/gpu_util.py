@@ -38,8 +38,11 @@ def config(w: gen.Workload, n_clusters: int, out_bf16=False, **over):
     return pk.config_for(out_bf16=out_bf16, **kw)
 
 
-def run_gpu(w: gen.Workload, data: dict, cs, dev, *, out_bf16=False, n_tokens=None, with_scores=True, **over):
-    """Whole path on the GPU; returns host copies of every output plus the call counter."""
+def run_gpu(w: gen.Workload, data: dict, cs, dev, *, out_bf16=False, n_tokens=None, with_scores=True, out_rows=None,
+            **over):
+    """Whole path on the GPU; returns host copies of every output plus the call counter.
+    With `out_rows`, only those rows of the attention output are copied back (res["out"][i] is
+    row out_rows[i])."""
     import torch
 
     import paper_2609_31568_amd as pk
@@ -55,11 +58,14 @@ def run_gpu(w: gen.Workload, data: dict, cs, dev, *, out_bf16=False, n_tokens=No
         pk.run_layer(h, q, kp, vp, bt, n, cs, bufs)
         torch.cuda.synchronize()
         calls = h.retrieval_calls()
+    out = bufs.out
+    if out_rows is not None:
+        out = out.index_select(0, torch.as_tensor(np.asarray(out_rows, dtype=np.int64), device=dev))
     res = {
         "k_rep": bufs.k_rep.cpu().numpy(),
         "sel_idx": bufs.sel_idx.cpu().numpy(),
         "sel_cnt": bufs.sel_cnt.cpu().numpy(),
-        "out": bufs.out.float().cpu().numpy() if not out_bf16 else bufs.out.view(torch.int16).cpu().numpy(),
+        "out": out.float().cpu().numpy() if not out_bf16 else out.view(torch.int16).cpu().numpy(),
         "calls": calls,
     }
     if with_scores:

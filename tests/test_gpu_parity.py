@@ -197,6 +197,62 @@ def test_full_size_llama(dev, name, seed_rows):
     gu.log(f"[parity] {name}: sampled attention worst max-abs {worst[0]:.2e} rel-L2 {worst[1]:.2e}")
 
 
+def _oracle_clusters(w, d, cs, clusters):
+    """The oracle's selection (Alg. 2's per-cluster steps) for the listed clusters only, with the
+    representative keys of every block they score; the same layout as oracle.prefill's result."""
+    geo = oracle.geometry(w.n_tokens, w.sub_chunk, w.block_size, w.sink_tokens, w.local_window, w.top_k, cs)
+    n_rep = max(geo[j].sink_blk + geo[j].n_cand for j in clusters)
+    k_rep = oracle.rep_keys(d["k_pages"], d["block_table"], w.n_tokens, w.block_size, blocks=np.arange(n_rep))
+    ref = {"geometry": [], "fingerprints": [], "scores": [], "selections": [], "margins": [], "k_rep": k_rep}
+    for j in clusters:
+        g = geo[j]
+        v = oracle.anchor_fingerprint(d["q"], g.s, g.anchor_end)
+        sc = oracle.soft_vote(oracle.block_logits(v, k_rep[g.sink_blk:g.sink_blk + g.n_cand], w.num_kv_heads))
+        sel, margin = oracle.select_topk(sc, g.sink_blk, w.top_k)
+        for key, val in (("geometry", g), ("fingerprints", v), ("scores", sc), ("selections", sel),
+                         ("margins", margin)):
+            ref[key].append(val)
+    return ref
+
+
+@pytest.mark.parametrize("name,layer,cluster,n_sample,seed", [("qwen256k", 27, 0, 12, 7), ("stress1m", 0, 1, 16, 8)])
+def test_full_size_sampled(dev, name, layer, cluster, n_sample, seed):
+    """Full-size Qwen2-7B-shaped layer (its last layer, G = 7) and the 1M context at cluster size 1:
+    the GPU runs the whole layer; a sample of clusters (first, last, random) is checked against the
+    oracle -- representative keys, fingerprints, scores, selection -- and their first and last
+    32-row tiles of attention."""
+    w = gen.WORKLOADS[name]
+    w = w.with_(cluster=cluster or w.cluster)
+    gu.log(f"[parity] {name} layer {layer} c={w.cluster}: generating")
+    d = gen.make_layer(w, layer)
+    cs = gen.cluster_starts(w.n_sub_chunks, w.cluster)
+    J = len(cs) - 1
+    rng = np.random.default_rng(seed)
+    clusters = sorted({0, J - 1, *rng.choice(np.arange(1, J - 1), size=n_sample - 2, replace=False).tolist()})
+    geo = oracle.geometry(w.n_tokens, w.sub_chunk, w.block_size, w.sink_tokens, w.local_window, w.top_k, cs)
+    rows = gu.sample_rows([geo[j] for j in clusters], rng, tiles_per_cluster=0)
+    gu.log(f"[parity] {name}: GPU, {J} clusters")
+    res = gu.run_gpu(w, d, cs, dev, out_rows=np.concatenate(rows))
+    assert res["calls"] == J
+    gu.log(f"[parity] {name}: oracle on clusters {clusters}")
+    ref = _oracle_clusters(w, d, cs, clusters)
+    gu.check_rounding(res["k_rep"][:len(ref["k_rep"])], ref["k_rep"], "k_rep")
+    gu.check_rounding(res["fingerprints"][clusters], np.stack(ref["fingerprints"]), "fingerprints")
+    worst = gu.check_scores(res["scores"][clusters], ref, w.num_kv_heads, name)
+    n_exact = gu.check_selection(res["sel_idx"][clusters], res["sel_cnt"][clusters], ref, EPS_VALID)
+    gu.log(f"[parity] {name}: worst score error {worst:.2e}; {n_exact} of {len(clusters)} sampled clusters above "
+           f"the margin, all equal")
+    sels = gu.gpu_selections(res, J)
+    worst, at = (0.0, 0.0), 0
+    for i, j in enumerate(clusters):
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], geo[j], sels[j], rows[i],
+                                      w.block_size)
+        mx, rel = gu.check_output(res["out"][at:at + len(rows[i])], o_ref, f"{name} cluster {j}")
+        at += len(rows[i])
+        worst = (max(worst[0], mx), max(worst[1], rel))
+    gu.log(f"[parity] {name}: sampled attention worst max-abs {worst[0]:.2e} rel-L2 {worst[1]:.2e}")
+
+
 def test_abi_errors_on_device(dev):
     """Invalid calls on a live handle return their status and launch nothing."""
     import ctypes
