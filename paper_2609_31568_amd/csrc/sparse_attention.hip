@@ -1,5 +1,5 @@
 // Gathered block-sparse flash attention for cluster-level sparse prefill (paper Sec. 5.1.3,
-// Eq. 10; Algorithm 2, "compute cluster attention ... with causal mask").
+// Eq. 10; the cluster attention step of Algorithm 2, causal).
 //
 // Work item = (cluster j, KV head g, tile of up to 32 * RB query positions). The work-group has
 // G * RB waves: one per (query head of the group, 32-position row block). All of them share the
@@ -24,19 +24,22 @@
 // 8 consecutive keys from each lane half, which the V^T operand reads as one 16-byte chunk.
 //
 // Order inside a tile: S(keys 0-31), S(keys 32-63), softmax(0-31), PV(0-31), softmax(32-63),
-// PV(32-63). MFMAs run asynchronously, so each half's VALU softmax overlaps the MFMAs issued
-// just before it (the other half's S, then the first half's PV) within the wave; the second wave
-// on the SIMD fills what is left.
+// PV(32-63). Each group of eight MFMAs has its eight LDS operand reads issued ahead of it. MFMAs
+// run asynchronously, so each half's VALU softmax overlaps the MFMAs issued just before it
+// within the wave; the second wave on the SIMD fills what is left.
 //
-// Pipelining: LDS holds two tile buffers. While a tile is consumed from one buffer, the next
-// tile's global loads are in flight into registers; they are written to the other buffer after
-// the MFMA work, and one barrier per tile separates the phases.
+// Pipelining: LDS holds two tile buffers, and two register sets stage the global loads. A tile's
+// loads are issued two tiles ahead; they are written to LDS at the end of the tile before it, and
+// one barrier per tile separates the phases.
 //
-// LDS layouts (conflict-free for the operand reads and the tile writes):
+// LDS layouts:
 //   K   [row][d], row stride d + 8 elements; row 32 b + 8 i + 4 h + j holds key 32 b + 16 h + 4 i + j
+//       (operand reads conflict-free)
 //   V^T [d][key], row stride 68 dwords; the 32 key-pair dwords of row d start at dword
-//       4 ((d / 8) % 8), so the transposing 32-bit writes of a 32-lane group (4 key pairs x 8
-//       d-chunks) hit 32 banks, and the 16-byte reads of 8 lanes (8 rows) do too.
+//       4 ((d / 8) % 8), which keeps the transposing 32-bit tile writes conflict-free. The 16-byte
+//       operand reads see 2-way conflicts for part of the lanes under gfx950's 64-bank,
+//       16-lanes-per-pass service of 16-byte reads; a fully conflict-free layout (36-dword rows
+//       with an xor swizzle) measured no faster.
 // (ds_read_b64_tr_b16 would avoid the transposing writes, but it sustains well under half the
 // bytes per clock of ds_read_b128, and the V operand reads dominate the LDS traffic.)
 #include <math.h>
@@ -220,12 +223,9 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     }
   };
 
-  // ---- per-thread prefetch registers for one K and one V tile ----
-  u32x4 kreg[S::kPer], vreg[2 * S::kVPer];
-#define SCALE_LOAD_TILE(T)                                                                       \
-  load_tile<S, D>(kreg, vreg, k_pages, v_pages,                                                  \
-                  (int64_t)tile_row[((T) / kDescBatch) & 1][(T) % kDescBatch] * D, tid)
-#define SCALE_STORE_TILE(BUF) store_tile<S, D>(kreg, vreg, lds + (BUF) * S::kBufElems, tid)
+  // ---- per-thread prefetch registers: two sets, each one K and one V tile ----
+  u32x4 kreg0[S::kPer], vreg0[2 * S::kVPer], kreg1[S::kPer], vreg1[2 * S::kVPer];
+  auto tile_base = [&](int t) -> int64_t { return (int64_t)tile_row[(t / kDescBatch) & 1][t % kDescBatch] * D; };
 
   // ---- Q fragments: B operand of S^T = K Q^T for each 16-wide slice of d ----
   bf16x8 qf[D / 16];
@@ -256,17 +256,22 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
   fill_batch(0);
   __syncthreads();
-  if (n_tiles > 0) {
-    SCALE_LOAD_TILE(0);
-    SCALE_STORE_TILE(0);
-  }
   if (n_tiles > kDescBatch) fill_batch(1);
+  // Tile j's global loads are issued two tiles ahead, in iteration j - 2, into register set j % 2,
+  // and stored into LDS buffer j % 2 at the end of iteration j - 1. Loads past the last tile
+  // re-read the last tile (never stored), which keeps the wait counts static.
+  if (n_tiles > 0) {
+    load_tile<S, D>(kreg0, vreg0, k_pages, v_pages, tile_base(0), tid);
+    store_tile<S, D>(kreg0, vreg0, lds, tid);
+    load_tile<S, D>(kreg1, vreg1, k_pages, v_pages, tile_base(min(1, n_tiles - 1)), tid);
+  }
   __syncthreads();
 
-  for (int t = 0; t < n_tiles; ++t) {
+  auto body = [&](int t, u32x4 (&kl)[S::kPer], u32x4 (&vl)[2 * S::kVPer], u32x4 (&ks)[S::kPer],
+                  u32x4 (&vs)[2 * S::kVPer]) {
     const int buf = t & 1;
     if (t > 0 && t % kDescBatch == 0 && t + kDescBatch < n_tiles) fill_batch(t / kDescBatch + 1);
-    if (t + 1 < n_tiles) SCALE_LOAD_TILE(t + 1);
+    load_tile<S, D>(kl, vl, k_pages, v_pages, tile_base(min(t + 2, n_tiles - 1)), tid);
 
     const uint16_t* k_lds = lds + buf * S::kBufElems;
     const uint16_t* v_lds = k_lds + S::kKElems;
@@ -276,12 +281,14 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const uint16_t* krow = k_lds + k_off + 32 * kb * S::kKStride;
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow), qf[0],
-                                                      f32x16{}, 0, 0, 0);
+      bf16x8 kf[D / 16];
 #pragma unroll
-      for (int c = 1; c < D / 16; ++c)
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(krow + 16 * c), qf[c],
-                                                        s[kb], 0, 0, 0);
+      for (int c = 0; c < D / 16; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(krow + 16 * c);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[0], f32x16{}, 0, 0, 0);
+#pragma unroll
+      for (int c = 1; c < D / 16; ++c) s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c], qf[c], s[kb], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, D / 16, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, D / 16, 0);
     }
 
     // Causal mask only on a local tile that reaches this wave's positions.
@@ -324,21 +331,27 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
       // O^T += V^T P^T over this half's two 16-key steps: step u takes keys 32kb + 16h + 8u + [0, 8)
       // from lane half h, which is entries [8u, 8u + 8) of s[kb] and one 16-byte V^T chunk.
+      bf16x8 vf[D / 32][2];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) vf[db][u] = *reinterpret_cast<const bf16x8*>(v_lds + vt_off[db] + 2 * (16 * kb + 4 * u));
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(v_lds + vt_off[db] + 2 * (16 * kb + 4 * u));
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[u], o[db], 0, 0, 0);
-        }
+        for (int u = 0; u < 2; ++u) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db][u], pf[u], o[db], 0, 0, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x100, D / 16, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, D / 16, 1);
     }
 
-    if (t + 1 < n_tiles) SCALE_STORE_TILE(buf ^ 1);
+    if (t + 1 < n_tiles) store_tile<S, D>(ks, vs, lds + (buf ^ 1) * S::kBufElems, tid);
     __syncthreads();
+  };
+  for (int t = 0; t < n_tiles; t += 2) {
+    body(t, kreg0, vreg0, kreg1, vreg1);
+    if (t + 1 < n_tiles) body(t + 1, kreg1, vreg1, kreg0, vreg0);
   }
-#undef SCALE_LOAD_TILE
-#undef SCALE_STORE_TILE
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
