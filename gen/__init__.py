@@ -56,9 +56,9 @@ def _load():
     lib.tg_bf16.argtypes = [ctypes.c_double]
     lib.tg_bf16.restype = ctypes.c_uint16
     lib.tg_topics.argtypes = [u64, i32, i32, i32, p]
-    lib.tg_query_topics.argtypes = [u64, i32, i32, i32, i32, i32, p]
+    lib.tg_query_topics.argtypes = [u64, i32, i32, i32, i32, i32, ctypes.c_double, ctypes.c_double, p, p]
     lib.tg_kv_topics.argtypes = [u64, i32, i32, i32, p]
-    lib.tg_fill_q.argtypes = [u64, i32, p, p, i32, i32, i32, i64, i64, p]
+    lib.tg_fill_q.argtypes = [u64, i32, p, p, p, i32, i32, i32, i64, i64, p]
     lib.tg_fill_kv.argtypes = [u64, i32, p, p, i32, i32, i32, i64, i64, p, p]
     _lib = lib
     return lib
@@ -84,6 +84,8 @@ class Workload:
     run_lo: int
     run_hi: int
     seed: int
+    q_scale_lo: float = 2.0   # topic strength of a query run, drawn uniformly in [lo, hi]
+    q_scale_hi: float = 2.0
 
     @property
     def n_blocks(self) -> int:
@@ -108,6 +110,11 @@ WORKLOADS = {
     "qwen256k": Workload("qwen256k", 28, 28, 4, 128, 262144, 128, 1024, 4, 32, 128, 8192, 512, 1, 8, 3),
     # Llama-3-8B layer at 1M context; the cluster size is swept over {1, 2, 4, 8, 16}
     "stress1m": Workload("stress1m", 1, 32, 8, 128, 1048576, 128, 512, 8, 64, 128, 4096, 2048, 1, 32, 4),
+    # the 128K layer with query runs of varying coherence (topic strength 2 .. 6, so same-topic
+    # sub-chunk fingerprints have cosines from about 0.94 to 0.993): the similarity-threshold
+    # clustering workload; its fixed cluster size (8) is the L_max / L cap of the paper's default
+    "scr128k": Workload("scr128k", 1, 32, 8, 128, 131072, 128, 512, 8, 32, 128, 4096, 256, 2, 16, 5,
+                        q_scale_lo=2.0, q_scale_hi=6.0),
 }
 
 
@@ -132,11 +139,18 @@ def topics(w: Workload, layer: int = 0) -> np.ndarray:
     return t
 
 
-def query_topics(w: Workload, layer: int = 0) -> np.ndarray:
+def query_runs(w: Workload, layer: int = 0):
+    """(topic, topic strength) of every sub-chunk: int32 [M], float64 [M]."""
     lib = _load()
     qt = np.empty(w.n_sub_chunks, dtype=np.int32)
-    lib.tg_query_topics(w.seed, layer, w.n_topics, w.run_lo, w.run_hi, w.n_sub_chunks, qt.ctypes.data)
-    return qt
+    qs = np.empty(w.n_sub_chunks, dtype=np.float64)
+    lib.tg_query_topics(w.seed, layer, w.n_topics, w.run_lo, w.run_hi, w.n_sub_chunks, float(w.q_scale_lo),
+                        float(w.q_scale_hi), qt.ctypes.data, qs.ctypes.data)
+    return qt, qs
+
+
+def query_topics(w: Workload, layer: int = 0) -> np.ndarray:
+    return query_runs(w, layer)[0]
 
 
 def kv_topics(w: Workload, layer: int = 0) -> np.ndarray:
@@ -146,17 +160,17 @@ def kv_topics(w: Workload, layer: int = 0) -> np.ndarray:
     return kt
 
 
-def q_rows(w: Workload, row0: int, n_rows: int, layer: int = 0, *, _topics=None, _qtopic=None,
+def q_rows(w: Workload, row0: int, n_rows: int, layer: int = 0, *, _topics=None, _qruns=None,
            out: np.ndarray | None = None) -> np.ndarray:
     """Q rows [row0, row0 + n_rows) as bf16 bits, shape [n_rows, Hq, d]."""
     lib = _load()
     t = topics(w, layer) if _topics is None else _topics
-    qt = query_topics(w, layer) if _qtopic is None else _qtopic
+    qt, qs = query_runs(w, layer) if _qruns is None else _qruns
     if row0 < 0 or row0 + n_rows > w.n_tokens:
         raise ValueError("row range outside the context")
     q = out if out is not None else np.empty((n_rows, w.num_q_heads, w.head_dim), dtype=np.uint16)
     assert q.shape == (n_rows, w.num_q_heads, w.head_dim) and q.dtype == np.uint16 and q.flags.c_contiguous
-    lib.tg_fill_q(w.seed, layer, t.ctypes.data, qt.ctypes.data, w.sub_chunk, w.num_q_heads,
+    lib.tg_fill_q(w.seed, layer, t.ctypes.data, qt.ctypes.data, qs.ctypes.data, w.sub_chunk, w.num_q_heads,
                   w.head_dim, row0, n_rows, q.ctypes.data)
     return q
 
@@ -187,9 +201,9 @@ def make_layer(w: Workload, layer: int = 0) -> dict:
     """All inputs of one layer: q [N, Hq, d], k_pages / v_pages [n_blocks, Hkv, B, d] (bf16 bits),
     identity block table, and the topic labels that generated them."""
     t = topics(w, layer)
-    qt = query_topics(w, layer)
+    qt, qs = query_runs(w, layer)
     kt = kv_topics(w, layer)
-    q = q_rows(w, 0, w.n_tokens, layer, _topics=t, _qtopic=qt)
+    q = q_rows(w, 0, w.n_tokens, layer, _topics=t, _qruns=(qt, qs))
     k, v = kv_blocks(w, 0, w.n_blocks, layer, _topics=t, _kvtopic=kt)
     return {
         "q": q,
@@ -197,6 +211,7 @@ def make_layer(w: Workload, layer: int = 0) -> dict:
         "v_pages": v,
         "block_table": np.arange(w.n_blocks, dtype=np.int32),
         "qtopic": qt,
+        "qscale": qs,
         "kvtopic": kt,
         "topics": t,
     }

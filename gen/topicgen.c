@@ -16,9 +16,11 @@
  *   topic vectors   T[i][c] = N(0,1) / sqrt(d),   i < n_topics, shared by every head
  *   query topics    a run-length process over sub-chunks: draw a topic uniformly, draw a run
  *                   length uniformly in [run_lo, run_hi], give that topic to the next run-length
- *                   sub-chunks (truncated at the last one), repeat
+ *                   sub-chunks (truncated at the last one), repeat; run r also draws a topic
+ *                   strength s_r uniformly in [s_lo, s_hi] from a stream of its own (s_lo = s_hi
+ *                   gives every run that strength exactly)
  *   KV block topics each block of B tokens draws its topic uniformly and independently
- *   Q[p][h][c]  = 2 T[qtopic(p / L)][c] + N(0,1)
+ *   Q[p][h][c]  = s(p / L) T[qtopic(p / L)][c] + N(0,1)   (s = the strength of the sub-chunk's run)
  *   K[t][g][c]  = 2 T[kvtopic(t / B)][c] + N(0,1)
  *   V[t][g][c]  = N(0,1)
  * Every value is rounded to fp32 (round-to-nearest-even) and then to bf16 (RNE); bf16 values are
@@ -31,7 +33,7 @@
 
 #define GOLDEN 0x9E3779B97F4A7C15ULL
 
-enum { T_TOPICS = 1, T_QTOPIC = 2, T_KVTOPIC = 3, T_QNOISE = 4, T_KNOISE = 5, T_V = 6 };
+enum { T_TOPICS = 1, T_QTOPIC = 2, T_KVTOPIC = 3, T_QNOISE = 4, T_KNOISE = 5, T_V = 6, T_QSCALE = 7 };
 
 static inline uint64_t mix64(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
@@ -99,16 +101,24 @@ void tg_topics(uint64_t seed, int layer, int n_topics, int d, double* topics) {
   for (int64_t i = 0; i < (int64_t)n_topics * d; ++i) topics[i] *= s;
 }
 
-/* qtopic[M]: topic of each sub-chunk from the run-length process. */
+/* qtopic[M], qscale[M]: topic and topic strength of each sub-chunk from the run-length process. */
 void tg_query_topics(uint64_t seed, int layer, int n_topics, int run_lo, int run_hi, int M,
-                     int32_t* qtopic) {
+                     double scale_lo, double scale_hi, int32_t* qtopic, double* qscale) {
   uint64_t key = tg_stream_key(seed, (uint64_t)layer, T_QTOPIC);
-  uint64_t n = 0;
+  uint64_t skey = tg_stream_key(seed, (uint64_t)layer, T_QSCALE);
+  uint64_t n = 0, run_index = 0;
   int m = 0;
   while (m < M) {
     int32_t topic = (int32_t)uniform_int(draw(key, n++), n_topics);
     int run = run_lo + (int)uniform_int(draw(key, n++), (int64_t)(run_hi - run_lo + 1));
-    for (int r = 0; r < run && m < M; ++r) qtopic[m++] = topic;
+    double s = scale_lo == scale_hi ? scale_lo
+                                    : scale_lo + (scale_hi - scale_lo) * uniform53(draw(skey, run_index));
+    ++run_index;
+    for (int r = 0; r < run && m < M; ++r) {
+      qtopic[m] = topic;
+      qscale[m] = s;
+      ++m;
+    }
   }
 }
 
@@ -119,8 +129,8 @@ void tg_kv_topics(uint64_t seed, int layer, int n_topics, int n_blocks, int32_t*
 }
 
 /* Q rows [row0, row0 + n_rows) as bf16 bits, row-major [row][Hq][d]. */
-void tg_fill_q(uint64_t seed, int layer, const double* topics, const int32_t* qtopic, int L,
-               int Hq, int d, int64_t row0, int64_t n_rows, uint16_t* q) {
+void tg_fill_q(uint64_t seed, int layer, const double* topics, const int32_t* qtopic,
+               const double* qscale, int L, int Hq, int d, int64_t row0, int64_t n_rows, uint16_t* q) {
   uint64_t key = tg_stream_key(seed, (uint64_t)layer, T_QNOISE);
   int64_t row_elems = (int64_t)Hq * d;
 #pragma omp parallel
@@ -130,12 +140,13 @@ void tg_fill_q(uint64_t seed, int layer, const double* topics, const int32_t* qt
     for (int64_t r = 0; r < n_rows; ++r) {
       int64_t p = row0 + r;
       const double* t = topics + (int64_t)qtopic[p / L] * d;
+      const double s = qscale[p / L];
       for (int64_t off = 0; off < row_elems; off += 2048) {
         int64_t cnt = row_elems - off < 2048 ? row_elems - off : 2048;
         normals(key, (uint64_t)(p * row_elems + off), cnt, buf);
         for (int64_t e = 0; e < cnt; ++e) {
           int c = (int)((off + e) % d);
-          q[r * row_elems + off + e] = to_bf16(2.0 * t[c] + buf[e]);
+          q[r * row_elems + off + e] = to_bf16(s * t[c] + buf[e]);
         }
       }
     }

@@ -22,6 +22,11 @@ equations (equation numbers in source order):
 * Sec. 5.1.3, Eq. 10: cluster attention over three key groups (the shared top-k set, the
   attention sinks, and a local window widened to span the whole cluster) under a causal mask.
 * Algorithm 2: per cluster, select -> augment with sink and local -> attend -> write.
+* Sec. 5.1.1: fingerprints are L2-normalised once, so a cosine is one inner product.
+* Sec. 5.1.2, Algorithm 1 with the admission rule of Eq. 8: anchor-based clustering of an outer
+  chunk's sub-chunks in one left-to-right pass; a sub-chunk joins the open cluster while its
+  cosine with the cluster's first sub-chunk (the anchor) reaches theta and the cluster is still
+  below L_max tokens, and otherwise becomes the next anchor.
 
 Readings where the paper is silent (block-level selection, the representative key, the
 candidate set, local-window geometry, tie-break), all named R-numbers below, are listed with
@@ -42,6 +47,11 @@ their reasons in the design notes:
       them all; the selection is emitted in ascending block order
   R13 causal: a key is visible to a query iff its position is <= the query's position
   R14 attention scale 1/sqrt(d_h) (Eqs. 1, 10) unless given
+  R20 clustering compares the fingerprints of all heads concatenated (Eq. 6's v_i in R^d); a
+      zero fingerprint has no direction, so its cosine is undefined (NaN) and never reaches theta
+  R21 the cap test |C| L < L_max counts whole sub-chunks of L rows (the last, short sub-chunk
+      too), so a cluster holds at most ceil(L_max / L) sub-chunks; clusters restart at each outer
+      chunk boundary when the outer chunk length is given
 """
 from __future__ import annotations
 
@@ -65,6 +75,9 @@ __all__ = [
     "cluster_attention",
     "prefill",
     "retrieval_calls",
+    "subchunk_fingerprints",
+    "normalized",
+    "anchor_clustering",
 ]
 
 
@@ -296,3 +309,50 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
         "retrieval_calls": len(geo),
         "degenerate": sum(1 for g in geo if g.n_cand <= top_k),
     }
+
+
+def subchunk_fingerprints(q, n_tokens: int, sub_chunk: int) -> np.ndarray:
+    """Eq. 6 for every sub-chunk of the outer chunk: v_i is the mean over the sub-chunk's rows of the
+    multi-head query, all heads concatenated (R20); the last sub-chunk may be short (Sec. 3.1).
+
+    ``q`` is [N, Hq, d] bf16 bits. Returns [M, Hq * d] fp64, M = ceil(N / L).
+    """
+    m = -(-n_tokens // sub_chunk)
+    out = np.empty((m, q.shape[1] * q.shape[2]), dtype=np.float64)
+    for i in range(m):
+        rows = bf16_to_f64(q[i * sub_chunk:min((i + 1) * sub_chunk, n_tokens)])
+        out[i] = rows.reshape(rows.shape[0], -1).sum(axis=0) / rows.shape[0]
+    return out
+
+
+def normalized(v) -> np.ndarray:
+    """Sec. 5.1.1: v / ||v||_2 per fingerprint (a zero fingerprint gives NaN, R20)."""
+    v = np.asarray(v, dtype=np.float64)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        return v / np.linalg.norm(v, axis=-1, keepdims=True)
+
+
+def anchor_clustering(vt, theta: float, sub_chunk: int, l_max: int, outer_subchunks: int = 0) -> np.ndarray:
+    """Algorithm 1 (Sec. 5.1.2): one left-to-right pass over the normalised fingerprints ``vt``.
+
+    The open cluster starts at anchor a; sub-chunk j joins while cos(v_a, v_j) = vt[a] . vt[j]
+    reaches ``theta`` and the cluster's current size |C| satisfies |C| * L < L_max (Eq. 8); the
+    first j that fails either test closes the cluster and becomes the next anchor. With
+    ``outer_subchunks`` > 0 the pass also closes a cluster at every outer-chunk boundary (R21).
+    Returns cluster_start as int32 [n_clusters + 1] in sub-chunk units (first 0, last M).
+    """
+    vt = np.asarray(vt, dtype=np.float64)
+    m = vt.shape[0]
+    starts = []
+    a = 0
+    while a < m:
+        starts.append(a)
+        end = m if outer_subchunks <= 0 else min(m, (a // outer_subchunks + 1) * outer_subchunks)
+        size = 1
+        j = a + 1
+        while j < end and float(vt[a] @ vt[j]) >= theta and size * sub_chunk < l_max:
+            size += 1
+            j += 1
+        a = j
+    starts.append(m)
+    return np.asarray(starts, dtype=np.int32)
