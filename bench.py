@@ -37,6 +37,12 @@ def parse_args():
     ap.add_argument("--workload", default="llama128k")
     ap.add_argument("--cluster", type=int, default=0, help="cluster size in sub-chunks (0: the workload's)")
     ap.add_argument("--sweep", default="", help="comma-separated cluster sizes; one JSON line each")
+    ap.add_argument("--theta", type=float, default=None,
+                    help="form the clusters on the GPU by anchor-based similarity clustering at this threshold "
+                         "(each step) instead of fixed runs of --cluster sub-chunks")
+    ap.add_argument("--theta-sweep", default="", help="comma-separated thresholds; one JSON line each")
+    ap.add_argument("--l-max", type=int, default=0, help="cluster cap in tokens for --theta (0: 8 sub-chunks)")
+    ap.add_argument("--outer", type=int, default=0, help="outer chunk in sub-chunks for --theta (0: whole context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
     ap.add_argument("--out-bf16", action="store_true")
@@ -160,28 +166,43 @@ def cpu_baseline(w, data, cs, geo, n_tiles, n_sel_clusters=32, seed=0):
     }
 
 
-def time_path(args, w, c, layers, dev):
-    """Times `args.steps` steps of the whole path (every layer) for cluster size c; returns the
-    result dict without the CPU baseline."""
+def time_path(args, w, c, layers, dev, theta=None):
+    """Times `args.steps` steps of the whole path (every layer) for cluster size c, or, with
+    `theta`, with the clusters formed on the GPU by the anchor-based clustering at every step;
+    returns the result dict without the CPU baseline."""
     import gen
     import paper_2609_31568_amd as pk
     import torch
 
-    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    l_max = args.l_max or 8 * w.sub_chunk
+    max_clusters = w.n_sub_chunks if theta is not None else len(gen.cluster_starts(w.n_sub_chunks, c)) - 1
     cfg = pk.config_for(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
                         block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=w.top_k, sink_tokens=w.sink_tokens,
-                        local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=len(cs) - 1,
+                        local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=max_clusters,
                         out_bf16=args.out_bf16)
+    h = pk.Scale(cfg)
+    if theta is None:
+        cs = gen.cluster_starts(w.n_sub_chunks, c)
+        layer_cs = [cs] * len(layers)
+    else:
+        layer_cs = [h.cluster_subchunks(q, w.n_tokens, theta, l_max, args.outer) for q, *_ in layers]
+        cs = layer_cs[0]
     geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
     work = geometry_work(w, geo)
-    h = pk.Scale(cfg)
     # one set of outputs shared by the layers: each layer's output is complete when its attention
     # call ends, and the next layer's calls are ordered after it on the stream
-    bufs = pk.LayerBuffers(cfg, w.n_tokens, len(cs) - 1, device=dev)
+    bufs = pk.LayerBuffers(cfg, w.n_tokens, max_clusters, device=dev)
 
     def step():
-        for q, kp, vp, bt in layers:
-            pk.run_layer(h, q, kp, vp, bt, w.n_tokens, cs, bufs)
+        for (q, kp, vp, bt), lcs in zip(layers, layer_cs):
+            if theta is not None:
+                h.rep_keys(kp, bt, w.n_tokens, bufs.k_rep)
+                lcs = h.cluster_subchunks(q, w.n_tokens, theta, l_max, args.outer)
+                h.select_cluster(q, w.n_tokens, bufs.k_rep, lcs, bufs.sel_idx, bufs.sel_cnt, bufs.scores,
+                                 bufs.fingerprints)
+                h.sparse_prefill(q, kp, vp, bt, w.n_tokens, lcs, bufs.sel_idx, bufs.sel_cnt, bufs.out)
+            else:
+                pk.run_layer(h, q, kp, vp, bt, w.n_tokens, lcs, bufs)
 
     for _ in range(args.warmup):
         step()
@@ -237,7 +258,8 @@ def time_path(args, w, c, layers, dev):
             "workload": f"{w.name}: {w.layers} x {shape}, {w.n_tokens} tokens",
             "n_tokens": w.n_tokens, "layers": w.layers, "num_q_heads": w.num_q_heads,
             "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": w.block_size,
-            "sub_chunk": w.sub_chunk, "cluster": c, "top_k": w.top_k, "sink_tokens": w.sink_tokens,
+            "sub_chunk": w.sub_chunk, "cluster": c if theta is None else f"anchor clustering, theta {theta}",
+            "top_k": w.top_k, "sink_tokens": w.sink_tokens,
             "local_window": w.local_window, "out_dtype": "bf16" if args.out_bf16 else "fp32",
             "seed": w.seed,
         },
@@ -248,7 +270,7 @@ def time_path(args, w, c, layers, dev):
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(w.name) if c == gen.WORKLOADS[w.name].cluster else None,
+            "traffic": measured_traffic(w.name) if theta is None and c == gen.WORKLOADS[w.name].cluster else None,
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
         },
@@ -259,7 +281,19 @@ def time_path(args, w, c, layers, dev):
         "retrieval_calls": {"per_step": int(calls), "per_layer": len(cs) - 1, "clusters": len(cs) - 1,
                             "per_sub_chunk_baseline": w.n_sub_chunks * w.layers,
                             "reduction": round(w.n_sub_chunks * w.layers / max(calls, 1), 2)},
+        **({"clustering": _cluster_stats(cs, theta, l_max, args.outer, w)} if theta is not None else {}),
     }, cs, geo
+
+
+def _cluster_stats(cs, theta, l_max, outer, w):
+    import numpy as np
+
+    sizes = np.diff(np.asarray(cs))
+    cap = -(-l_max // w.sub_chunk)
+    hist = np.bincount(sizes, minlength=cap + 1)[1:cap + 1]
+    return {"theta": theta, "l_max_tokens": l_max, "outer_subchunks": outer, "clusters": int(len(sizes)),
+            "mean_size_tokens": round(float(sizes.mean() * w.sub_chunk), 1),
+            "size_fraction": {str(i + 1): round(float(x) / len(sizes), 4) for i, x in enumerate(hist)}}
 
 
 def main():
@@ -306,10 +340,13 @@ def main():
         del data
     print(f"[bench] inputs ready in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
 
-    for c in sweep:
+    thetas = [float(x) for x in args.theta_sweep.split(",")] if args.theta_sweep else (
+        [args.theta] if args.theta is not None else [])
+    runs = [(w.cluster, t) for t in thetas] if thetas else [(c, None) for c in sweep]
+    for c, theta in runs:
         wc = w.with_(cluster=c)
-        print(f"[bench] timing c={c}", file=sys.stderr, flush=True)
-        result, cs, geo = time_path(args, wc, c, layers, dev)
+        print(f"[bench] timing " + (f"theta={theta}" if theta is not None else f"c={c}"), file=sys.stderr, flush=True)
+        result, cs, geo = time_path(args, wc, c, layers, dev, theta=theta)
         if rank == 0 and not args.no_cpu_baseline:
             print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
             result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles)

@@ -135,6 +135,28 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
                                   int32_t n_clusters, const int32_t* sel_idx,
                                   const int32_t* sel_cnt, void* out);
 
+/* Anchor-based clustering of the sub-chunks of an outer chunk (Sec. 5.1.1-5.1.2, Algorithm 1,
+ * Eq. 8), producing the cluster_start the calls above take. For every sub-chunk i (rows
+ * [i L, min((i + 1) L, n_tokens)), M = ceil(n_tokens / L) of them) the fingerprint v_i is the mean
+ * of its query rows over all heads concatenated (Eq. 6, in R^(Hq d)). One left-to-right pass then
+ * forms the clusters: a cluster opens at anchor a and admits the next sub-chunk j while
+ * cos(v_a, v_j) >= theta and the cluster holds |C| sub-chunks with |C| * L < l_max; the first j
+ * failing either test opens the next cluster. With outer_subchunks > 0, a cluster also closes at
+ * every multiple of outer_subchunks (clusters never span two outer chunks). Everything is fp64;
+ * a zero fingerprint has an undefined (NaN) cosine and never joins or admits.
+ *   q             device bf16 [n_tokens][Hq][d], 0 < n_tokens <= max_tokens
+ *   theta         similarity threshold (any value but NaN; > 1 gives single sub-chunks)
+ *   l_max         cluster cap in tokens, >= 1 (the paper's default is 8 L)
+ *   cluster_start HOST int32 with room for M + 1 entries: receives 0, ..., M
+ *   n_clusters    HOST: receives the number of clusters
+ *   cos_band      optional HOST double [M][span]: cos(v_i, v_{i+o}) at [i][o - 1], NaN past the last
+ *                 sub-chunk; span = min(ceil(l_max / L), outer_subchunks if > 0, M) - 1
+ * span above 64 returns SCALE_ERR_UNSUPPORTED. Synchronous: waits for the handle's stream. The
+ * result does not count as a selection call. */
+scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, double theta,
+                                     int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
+                                     int32_t* n_clusters, double* cos_band);
+
 /* Static text for a status code. Never NULL. */
 const char* scale_status_string(scale_status s);
 
@@ -148,7 +170,8 @@ typedef enum {
   SCALE_STAGE_LOGITS = 2,       /* per-head block logits                                 */
   SCALE_STAGE_VOTE_TOPK = 3,    /* soft-voting scores and top-k                          */
   SCALE_STAGE_ATTENTION = 4,    /* block-sparse attention                                */
-  SCALE_NUM_STAGES = 5
+  SCALE_STAGE_CLUSTER = 5,      /* sub-chunk similarity of scale_cluster_subchunks        */
+  SCALE_NUM_STAGES = 6
 } scale_stage;
 
 /* Device-time instrumentation (off by default). While enabled, every stage's kernels of every

@@ -26,9 +26,9 @@ SCALE_OUT_BF16 = 1
 EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
-    "scale_stage_times",
+    "scale_stage_times", "scale_cluster_subchunks",
 )
-STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention")
+STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster")
 
 
 class ScaleError(RuntimeError):
@@ -80,6 +80,8 @@ def _load():
     lib.scale_enable_timing.restype = ctypes.c_int
     lib.scale_stage_times.argtypes = [vp, vp, vp, ctypes.c_int]
     lib.scale_stage_times.restype = ctypes.c_int
+    lib.scale_cluster_subchunks.argtypes = [vp, vp, i32, ctypes.c_double, i32, i32, vp, vp, vp]
+    lib.scale_cluster_subchunks.restype = ctypes.c_int
     return lib
 
 
@@ -187,6 +189,24 @@ class Scale:
                                         _ptr(out)),
                "scale_sparse_prefill")
 
+    def cluster_subchunks(self, q, n_tokens: int, theta: float, l_max: int, outer_subchunks: int = 0,
+                          with_band: bool = False):
+        """Anchor-based clustering of the sub-chunks; returns cluster_start (int32 [n + 1]) and, with
+        ``with_band``, the cosine band [M][span] (see include/scale.h)."""
+        L = self.cfg.sub_chunk
+        m = -(-int(n_tokens) // L)
+        cs = np.zeros(m + 1, dtype=np.int32)
+        n = ctypes.c_int32()
+        band = None
+        if with_band:
+            band = np.full((m, cluster_span(l_max, L, outer_subchunks, m)), np.nan, dtype=np.float64)
+        _check(lib.scale_cluster_subchunks(self._h, _ptr(q), int(n_tokens), float(theta), int(l_max),
+                                           int(outer_subchunks), cs.ctypes.data, ctypes.byref(n),
+                                           None if band is None or band.size == 0 else band.ctypes.data),
+               "scale_cluster_subchunks")
+        cs = cs[:n.value + 1].copy()
+        return (cs, band) if with_band else cs
+
     def enable_timing(self, enable: bool = True):
         _check(lib.scale_enable_timing(self._h, 1 if enable else 0), "scale_enable_timing")
 
@@ -227,3 +247,15 @@ def scale_sparse_prefill(h: Scale, q, k_pages, v_pages, block_table, n_tokens, c
 
 def scale_retrieval_calls(h: Scale) -> int:
     return h.retrieval_calls()
+
+
+def scale_cluster_subchunks(h: Scale, q, n_tokens, theta, l_max, outer_subchunks=0, with_band=False):
+    return h.cluster_subchunks(q, n_tokens, theta, l_max, outer_subchunks, with_band)
+
+
+def cluster_span(l_max: int, sub_chunk: int, outer_subchunks: int, m: int) -> int:
+    """Width of the cosine band of scale_cluster_subchunks (include/scale.h)."""
+    cap = -(-int(l_max) // int(sub_chunk))
+    if outer_subchunks > 0:
+        cap = min(cap, int(outer_subchunks))
+    return min(cap, int(m)) - 1

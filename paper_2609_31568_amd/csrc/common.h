@@ -57,6 +57,14 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
                             int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                             hipStream_t stream);
 
+// Sub-chunk similarity for the anchor-based clustering: fp64 fingerprints [M][Hq * d] of every
+// sub-chunk, their inverse norms [M], and band[i][o - 1] = cos(v_i, v_{i+o}) for o = 1 .. span
+// (NaN past the last sub-chunk), M = ceil(n_tokens / sub_chunk).
+hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int sub_chunk, int num_q_heads,
+                                      int head_dim, int span, double* fingerprints, double* inv_norm,
+                                      double* band, hipStream_t stream);
+constexpr int kMaxClusterSpan = 64;   // largest band width (cluster cap - 1) the library supports
+
 // Block-sparse attention over the work list.
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,

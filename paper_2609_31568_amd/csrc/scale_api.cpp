@@ -51,6 +51,13 @@ struct scale_ctx {
   float* d_fingerprints = nullptr;
   float* d_logits = nullptr;
   float* d_spill = nullptr;
+  // sub-chunk clustering: fp64 fingerprints, inverse norms, cosine band (device) and the band's
+  // pinned host copy
+  int max_subchunks = 0;
+  double* d_sub_fp = nullptr;
+  double* d_inv_norm = nullptr;
+  double* d_band = nullptr;
+  double* h_band = nullptr;
   // pinned staging ring
   size_t slot_bytes = 0;
   Slot slots[kRingSlots];
@@ -163,6 +170,10 @@ void release(scale_ctx* h) {
   (void)hipFree(h->d_fingerprints);
   (void)hipFree(h->d_logits);
   (void)hipFree(h->d_spill);
+  (void)hipFree(h->d_sub_fp);
+  (void)hipFree(h->d_inv_norm);
+  (void)hipFree(h->d_band);
+  if (h->h_band) (void)hipHostFree(h->h_band);
   delete h;
 }
 
@@ -235,6 +246,7 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
   if (hipGetDevice(&h->device) != hipSuccess) { release(h); return SCALE_ERR_HIP; }
   const scale_config& c = h->cfg;
   h->max_blocks = (c.max_tokens + c.block_size - 1) / c.block_size;
+  h->max_subchunks = (c.max_tokens + c.sub_chunk - 1) / c.sub_chunk;
   h->max_items = (int)max_work_items(c);
   const int64_t row_elems = (int64_t)c.num_q_heads * c.head_dim;
   const int64_t mc = c.max_clusters;
@@ -248,7 +260,12 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
             dev((void**)&h->d_head_stats, sizeof(float2) * mc * c.num_q_heads * scale::selection_chunks(h->max_blocks)) &&
             dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
             dev((void**)&h->d_logits, sizeof(float) * mc * c.num_q_heads * (int64_t)h->max_blocks) &&
-            dev((void**)&h->d_spill, h->max_blocks > 8192 ? sizeof(float) * mc * h->max_blocks : 0);
+            dev((void**)&h->d_spill, h->max_blocks > 8192 ? sizeof(float) * mc * h->max_blocks : 0) &&
+            dev((void**)&h->d_sub_fp, sizeof(double) * (size_t)h->max_subchunks * row_elems) &&
+            dev((void**)&h->d_inv_norm, sizeof(double) * (size_t)h->max_subchunks) &&
+            dev((void**)&h->d_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan) &&
+            hipHostMalloc((void**)&h->h_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan,
+                          hipHostMallocDefault) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
     release(h);
@@ -329,6 +346,60 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
   h->retrieval_calls += n_clusters;
+  return SCALE_OK;
+}
+
+// Width of the cosine band: the largest number of sub-chunks a cluster may hold, minus one.
+static int32_t cluster_span(int32_t l_max, int32_t sub_chunk, int32_t outer_subchunks, int32_t m) {
+  int64_t cap = ((int64_t)l_max + sub_chunk - 1) / sub_chunk;
+  if (outer_subchunks > 0) cap = std::min<int64_t>(cap, outer_subchunks);
+  cap = std::min<int64_t>(cap, m);
+  return (int32_t)(cap - 1);
+}
+
+scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, double theta,
+                                     int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
+                                     int32_t* n_clusters, double* cos_band) {
+  if (!h || !q || !cluster_start || !n_clusters) return SCALE_ERR_INVALID_ARG;
+  if (n_tokens < 1 || std::isnan(theta) || l_max < 1 || outer_subchunks < 0) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
+  const int32_t L = c.sub_chunk;
+  const int32_t m = (n_tokens + L - 1) / L;
+  const int32_t span = cluster_span(l_max, L, outer_subchunks, m);
+  if (span > scale::kMaxClusterSpan) return SCALE_ERR_UNSUPPORTED;
+
+  stage_begin(h);
+  scale_status st = check_launch(scale::launch_subchunk_similarity(q, n_tokens, L, c.num_q_heads, c.head_dim, span,
+                                                                   h->d_sub_fp, h->d_inv_norm, h->d_band, h->stream));
+  if (st == SCALE_OK && span > 0 &&
+      hipMemcpyAsync(h->h_band, h->d_band, sizeof(double) * (size_t)m * span, hipMemcpyDeviceToHost, h->stream) !=
+          hipSuccess)
+    st = SCALE_ERR_HIP;
+  stage_end(h, SCALE_STAGE_CLUSTER);
+  if (st != SCALE_OK) return st;
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return SCALE_ERR_HIP;
+
+  // Algorithm 1: the open cluster starts at anchor a and admits j while cos(v_a, v_j) >= theta and
+  // the cluster holds fewer than ceil(l_max / L) sub-chunks (|C| L < l_max, Eq. 8); it also closes
+  // at an outer-chunk boundary. j - a - 1 < span always holds in the loop.
+  const int64_t cap = ((int64_t)l_max + L - 1) / L;
+  int32_t k = 0;
+  int32_t a = 0;
+  while (a < m) {
+    cluster_start[k++] = a;
+    const int32_t end = outer_subchunks > 0 ? std::min(m, (a / outer_subchunks + 1) * outer_subchunks) : m;
+    int64_t size = 1;
+    int32_t j = a + 1;
+    while (j < end && size < cap && h->h_band[(int64_t)a * span + (j - a - 1)] >= theta) {
+      ++size;
+      ++j;
+    }
+    a = j;
+  }
+  cluster_start[k] = m;
+  *n_clusters = k;
+  if (cos_band && span > 0) std::memcpy(cos_band, h->h_band, sizeof(double) * (size_t)m * span);
   return SCALE_OK;
 }
 

@@ -88,7 +88,22 @@ def test_calls_reject_null_handle():
     assert lib.scale_sparse_prefill(None, 1, 1, 1, None, 128, cs.ctypes.data, 1, 1, 1, 1) == -1
     n = ctypes.c_int64()
     assert lib.scale_retrieval_calls(None, ctypes.byref(n)) == -1
+    out = np.zeros(4, dtype=np.int32)
+    k = ctypes.c_int32()
+    assert lib.scale_cluster_subchunks(None, 1, 128, 0.95, 4096, 0, out.ctypes.data, ctypes.byref(k), None) == -1
     lib.scale_free(None)        # no-op
+
+
+def test_cluster_span_rule():
+    """Band width of scale_cluster_subchunks: the cluster cap in sub-chunks, bounded by the outer
+    chunk and the sub-chunk count, minus one."""
+    pk = _pk()
+    assert pk.cluster_span(4096, 512, 0, 256) == 7
+    assert pk.cluster_span(4097, 512, 0, 256) == 8
+    assert pk.cluster_span(4096, 512, 4, 256) == 3
+    assert pk.cluster_span(10 ** 9, 512, 16, 256) == 15
+    assert pk.cluster_span(10 ** 9, 512, 0, 5) == 4
+    assert pk.cluster_span(100, 512, 0, 256) == 0
 
 
 @pytest.mark.parametrize("name,c", [("tiny", 4), ("tiny", 1), ("llama32k", 8), ("llama128k", 8),

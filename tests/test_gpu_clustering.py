@@ -1,0 +1,156 @@
+"""GPU parity of the anchor-based clustering (paper Sec. 5.1.1-5.1.2, Algorithm 1, Eq. 8): the
+library's scale_cluster_subchunks against the fp64 oracle on the same seeded inputs, then the
+whole path driven by the clusters it forms."""
+import math
+
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+# GPU and oracle cosines differ by rounding only (fp64 on both sides); decisions are compared
+# exactly unless a cosine on the decision path lies this close to theta (none do on these inputs).
+COS_TOL = 1e-12
+NEAR = 1e-9
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_31568_amd  # noqa: F401
+
+    return torch.device("cuda:0")
+
+
+def _oracle_band(vt, span):
+    m = len(vt)
+    band = np.full((m, span), np.nan)
+    for i in range(m):
+        for o in range(1, span + 1):
+            if i + o < m:
+                band[i, o - 1] = vt[i] @ vt[i + o]
+    return band
+
+
+def _decision_cosines(starts, vt, theta, span):
+    """Cosines Algorithm 1 compares with theta for this partition (members and closing tests)."""
+    out = []
+    for a, e in zip(starts[:-1], starts[1:]):
+        for j in range(a + 1, min(e + 1, len(vt), a + span + 1)):
+            out.append(vt[a] @ vt[j])
+    return np.asarray(out)
+
+
+def _run(w, d, dev, theta, l_max, outer=0):
+    import paper_2609_31568_amd as pk
+
+    cfg = gu.config(w, w.n_sub_chunks)
+    q = gu.to_dev(d["q"], dev)
+    with pk.Scale(cfg) as h:
+        cs, band = h.cluster_subchunks(q, w.n_tokens, theta, l_max, outer, with_band=True)
+        calls = h.retrieval_calls()
+    assert calls == 0
+    return cs, band
+
+
+CASES = [
+    # workload overrides, theta, l_max in sub-chunks, outer sub-chunks
+    (dict(), 0.80, 4, 0),
+    (dict(q_scale_lo=2.0, q_scale_hi=6.0), 0.95, 8, 0),
+    (dict(q_scale_lo=2.0, q_scale_hi=6.0), 0.97, 8, 4),
+    (dict(q_scale_lo=2.0, q_scale_hi=6.0, n_tokens=2368), 0.90, 3, 0),     # short last sub-chunk
+    (dict(num_q_heads=8, num_kv_heads=2, head_dim=128, block_size=128, sub_chunk=512, n_tokens=16384,
+          q_scale_lo=1.0, q_scale_hi=6.0, run_lo=1, run_hi=6, n_topics=12), 0.93, 16, 0),
+]
+
+
+@pytest.mark.parametrize("over,theta,cap,outer", CASES)
+def test_clusters_match_oracle(dev, over, theta, cap, outer):
+    w = gen.WORKLOADS["tiny"].with_(**over)
+    gu.log(f"[clustering] {over} theta={theta} cap={cap} outer={outer}")
+    d = gen.make_layer(w)
+    l_max = cap * w.sub_chunk
+    cs, band = _run(w, d, dev, theta, l_max, outer)
+    vt = oracle.normalized(oracle.subchunk_fingerprints(d["q"], w.n_tokens, w.sub_chunk))
+    ref = oracle.anchor_clustering(vt, theta, w.sub_chunk, l_max, outer)
+    m = len(vt)
+    span = band.shape[1]
+    assert span == min(cap, outer if outer else m, m) - 1
+    ob = _oracle_band(vt, span)
+    assert np.array_equal(np.isnan(band), np.isnan(ob))
+    assert np.nanmax(np.abs(band - ob)) <= COS_TOL
+    assert np.all(np.abs(_decision_cosines(ref, vt, theta, span) - theta) > NEAR)
+    assert np.array_equal(cs, ref), f"{cs} != {ref}"
+    gu.log(f"[clustering] {len(ref) - 1} clusters of {m} sub-chunks; max band error "
+           f"{np.nanmax(np.abs(band - ob)):.1e}")
+
+
+def test_clustering_edge_cases(dev):
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = gen.WORKLOADS["tiny"].with_(q_scale_lo=3.0, q_scale_hi=3.0, run_lo=8, run_hi=8, n_topics=1)
+    d = gen.make_layer(w)
+    q = d["q"].copy()
+    q[3 * w.sub_chunk:4 * w.sub_chunk] = 0                      # sub-chunk 3 has a zero fingerprint
+    vt = oracle.normalized(oracle.subchunk_fingerprints(q, w.n_tokens, w.sub_chunk))
+    cfg = gu.config(w, w.n_sub_chunks)
+    qd = gu.to_dev(q, dev)
+    with pk.Scale(cfg) as h:
+        for theta, cap, outer in ((0.5, 8, 0), (1.5, 8, 0), (-math.inf, 3, 0), (0.5, 8, 5)):
+            cs = h.cluster_subchunks(qd, w.n_tokens, theta, cap * w.sub_chunk, outer)
+            ref = oracle.anchor_clustering(vt, theta, w.sub_chunk, cap * w.sub_chunk, outer)
+            assert np.array_equal(cs, ref), (theta, cap, outer, cs, ref)
+        assert np.array_equal(h.cluster_subchunks(qd, w.n_tokens, 0.5, 8 * w.sub_chunk), [0, 3, 4, 8])
+        # a band wider than 64 is refused before any launch; NaN theta is invalid
+        cs = np.zeros(9, dtype=np.int32)
+        n = __import__("ctypes").c_int32()
+        big = pk.Scale(gu.config(w.with_(n_tokens=2048 * 64, sub_chunk=64), 2048))
+        with big:
+            qb = torch.zeros((2048 * 64, w.num_q_heads, w.head_dim), dtype=torch.int16, device=dev)
+            with pytest.raises(pk.ScaleError) as e:
+                big.cluster_subchunks(qb, 2048 * 64, 0.9, 66 * 64)
+            assert e.value.status == pk.SCALE_ERR_UNSUPPORTED
+        assert pk.lib.scale_cluster_subchunks(h.handle, qd.data_ptr(), w.n_tokens, float("nan"), 4096, 0,
+                                              cs.ctypes.data, __import__("ctypes").byref(n), None) == \
+            pk.SCALE_ERR_INVALID_ARG
+
+
+def test_path_driven_by_gpu_clusters(dev):
+    """scr128k: the GPU forms the clusters at theta = 0.95, L_max = 8 L; selection and attention
+    then run on them, checked like the fixed-cluster full-size test (every selection, sampled
+    attention rows)."""
+    w = gen.WORKLOADS["scr128k"]
+    gu.log("[clustering] scr128k: generating")
+    d = gen.make_layer(w)
+    cs, band = _run(w, d, dev, 0.95, 8 * w.sub_chunk)
+    vt = oracle.normalized(oracle.subchunk_fingerprints(d["q"], w.n_tokens, w.sub_chunk))
+    ref_cs = oracle.anchor_clustering(vt, 0.95, w.sub_chunk, 8 * w.sub_chunk)
+    assert np.all(np.abs(_decision_cosines(ref_cs, vt, 0.95, 7) - 0.95) > NEAR)
+    assert np.array_equal(cs, ref_cs)
+    sizes = np.diff(cs)
+    gu.log(f"[clustering] scr128k theta 0.95: {len(sizes)} clusters, mean size {sizes.mean():.2f} sub-chunks, "
+           f"{np.mean(sizes == 8):.0%} at the cap")
+    assert 1 < len(sizes) < w.n_sub_chunks
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, sub_chunk=w.sub_chunk,
+                         block_size=w.block_size, top_k=w.top_k, sink_tokens=w.sink_tokens,
+                         local_window=w.local_window, cluster_start=cs, with_output=False)
+    gu.check_scores(res["scores"], ref, w.num_kv_heads, "scr128k")
+    gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, 1e-5)
+    rows = gu.sample_rows(ref["geometry"], np.random.default_rng(12), tiles_per_cluster=0)
+    sels = gu.gpu_selections(res, len(cs) - 1)
+    picks = np.random.default_rng(13).choice(len(cs) - 1, size=min(12, len(cs) - 1), replace=False)
+    for j in sorted(picks.tolist()):
+        g = ref["geometry"][j]
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j], rows[j],
+                                      w.block_size)
+        gu.check_output(res["out"][rows[j]], o_ref, f"scr128k cluster {j}")
