@@ -47,11 +47,12 @@ their reasons in the design notes:
       them all; the selection is emitted in ascending block order
   R13 causal: a key is visible to a query iff its position is <= the query's position
   R14 attention scale 1/sqrt(d_h) (Eqs. 1, 10) unless given
-  R20 clustering compares the fingerprints of all heads concatenated (Eq. 6's v_i in R^d); a
+  R22 clustering compares the fingerprints of all heads concatenated (Eq. 6's v_i in R^d); a
       zero fingerprint has no direction, so its cosine is undefined (NaN) and never reaches theta
-  R21 the cap test |C| L < L_max counts whole sub-chunks of L rows (the last, short sub-chunk
+  R23 the cap test |C| L < L_max counts whole sub-chunks of L rows (the last, short sub-chunk
       too), so a cluster holds at most ceil(L_max / L) sub-chunks; clusters restart at each outer
       chunk boundary when the outer chunk length is given
+  R24 the threshold test is taken in fp64
 """
 from __future__ import annotations
 
@@ -313,7 +314,7 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
 
 def subchunk_fingerprints(q, n_tokens: int, sub_chunk: int) -> np.ndarray:
     """Eq. 6 for every sub-chunk of the outer chunk: v_i is the mean over the sub-chunk's rows of the
-    multi-head query, all heads concatenated (R20); the last sub-chunk may be short (Sec. 3.1).
+    multi-head query, all heads concatenated (R22); the last sub-chunk may be short (Sec. 3.1).
 
     ``q`` is [N, Hq, d] bf16 bits. Returns [M, Hq * d] fp64, M = ceil(N / L).
     """
@@ -326,7 +327,7 @@ def subchunk_fingerprints(q, n_tokens: int, sub_chunk: int) -> np.ndarray:
 
 
 def normalized(v) -> np.ndarray:
-    """Sec. 5.1.1: v / ||v||_2 per fingerprint (a zero fingerprint gives NaN, R20)."""
+    """Sec. 5.1.1: v / ||v||_2 per fingerprint (a zero fingerprint gives NaN, R22)."""
     v = np.asarray(v, dtype=np.float64)
     with np.errstate(invalid="ignore", divide="ignore"):
         return v / np.linalg.norm(v, axis=-1, keepdims=True)
@@ -338,7 +339,7 @@ def anchor_clustering(vt, theta: float, sub_chunk: int, l_max: int, outer_subchu
     The open cluster starts at anchor a; sub-chunk j joins while cos(v_a, v_j) = vt[a] . vt[j]
     reaches ``theta`` and the cluster's current size |C| satisfies |C| * L < L_max (Eq. 8); the
     first j that fails either test closes the cluster and becomes the next anchor. With
-    ``outer_subchunks`` > 0 the pass also closes a cluster at every outer-chunk boundary (R21).
+    ``outer_subchunks`` > 0 the pass also closes a cluster at every outer-chunk boundary (R23).
     Returns cluster_start as int32 [n_clusters + 1] in sub-chunk units (first 0, last M).
     """
     vt = np.asarray(vt, dtype=np.float64)
