@@ -43,6 +43,8 @@ def parse_args():
     ap.add_argument("--theta-sweep", default="", help="comma-separated thresholds; one JSON line each")
     ap.add_argument("--l-max", type=int, default=0, help="cluster cap in tokens for --theta (0: 8 sub-chunks)")
     ap.add_argument("--outer", type=int, default=0, help="outer chunk in sub-chunks for --theta (0: whole context)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="also report the top-k overlap ratio (Eq. 7) of the clusters against per-sub-chunk selection")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
     ap.add_argument("--out-bf16", action="store_true")
@@ -218,6 +220,7 @@ def time_path(args, w, c, layers, dev, theta=None):
     t1 = time.perf_counter()
     stages = h.stage_times(reset=True)
     calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
+    overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap else None
     h.close()
     del bufs
 
@@ -282,7 +285,41 @@ def time_path(args, w, c, layers, dev, theta=None):
                             "per_sub_chunk_baseline": w.n_sub_chunks * w.layers,
                             "reduction": round(w.n_sub_chunks * w.layers / max(calls, 1), 2)},
         **({"clustering": _cluster_stats(cs, theta, l_max, args.outer, w)} if theta is not None else {}),
+        **({"topk_overlap": overlap} if overlap is not None else {}),
     }, cs, geo
+
+
+def overlap_stats(h, bufs, w, layer, cs):
+    """Eq. 7 for every cluster of layer 0: the cluster's selected blocks against the union of its
+    member sub-chunks' own selections (each over its single-sub-chunk candidate range), from two
+    selection calls on the GPU; min / median / mean / max over the clusters with a selection."""
+    import numpy as np
+    import torch
+
+    q, kp, vp, bt = layer
+    h.rep_keys(kp, bt, w.n_tokens, bufs.k_rep)
+    k = len(cs) - 1
+    h.select_cluster(q, w.n_tokens, bufs.k_rep, cs, bufs.sel_idx[:k], bufs.sel_cnt[:k])
+    torch.cuda.synchronize()
+    idx, cnt = bufs.sel_idx.cpu().numpy(), bufs.sel_cnt.cpu().numpy()
+    sel_c = [set(idx[j, :cnt[j]].tolist()) for j in range(k)]
+    m = w.n_sub_chunks
+    if bufs.sel_idx.shape[0] < m:
+        return {"note": "needs max_clusters >= the sub-chunk count (run with --theta or --cluster 1)"}
+    h.select_cluster(q, w.n_tokens, bufs.k_rep, np.arange(m + 1, dtype=np.int32), bufs.sel_idx, bufs.sel_cnt)
+    torch.cuda.synchronize()
+    idx, cnt = bufs.sel_idx.cpu().numpy(), bufs.sel_cnt.cpu().numpy()
+    rho = []
+    for j in range(k):
+        if not sel_c[j]:
+            continue
+        union = set()
+        for i in range(cs[j], cs[j + 1]):
+            union |= set(idx[i, :cnt[i]].tolist())
+        rho.append(len(sel_c[j] & union) / len(sel_c[j]))
+    rho = np.asarray(rho)
+    return {"clusters": int(len(rho)), "min": round(float(rho.min()), 4), "median": round(float(np.median(rho)), 4),
+            "mean": round(float(rho.mean()), 4), "max": round(float(rho.max()), 4)}
 
 
 def _cluster_stats(cs, theta, l_max, outer, w):

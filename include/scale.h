@@ -104,14 +104,22 @@ void scale_free(scale_handle h);
 scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32_t* block_table,
                             int32_t n_tokens, float* k_rep);
 
+/* scale_rep_keys for the logical blocks [first_block, n_tokens / B) only, leaving the other rows of
+ * k_rep as they are: the incremental form for the outer-chunk loop of Sec. 3.1, where each outer
+ * chunk appends blocks to the cache. Requires 0 <= first_block <= n_tokens / B. */
+scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const int32_t* block_table,
+                                  int32_t first_block, int32_t n_tokens, float* k_rep);
+
 /* Cluster-level selection (Eq. 9 with head soft-voting, Sec. 5.1.3), once per cluster:
  *   v[h]     = mean of q[p][h] over the anchor rows                      (Eq. 6 on the anchor)
  *   x[h][b]  = score_scale * v[h] . k_rep[b][g(h)]      for candidate blocks b
  *   score[b] = sum over h of softmax over candidates of x[h][.]   evaluated at b
  *   sel      = top sel_cnt candidates by (score descending, block index ascending), emitted in
  *              ascending block order into sel_idx[j][0..sel_cnt), the rest of the row is -1.
- * cluster_start: HOST int32[n_clusters + 1], cluster_start[0] = 0, strictly increasing,
- *   cluster_start[n_clusters] = ceil(n_tokens / sub_chunk).
+ * cluster_start: HOST int32[n_clusters + 1], strictly increasing, cluster_start[0] >= 0,
+ *   cluster_start[n_clusters] = ceil(n_tokens / sub_chunk). cluster_start[0] > 0 is incremental
+ *   prefill (the outer-chunk loop of Sec. 3.1): only the sub-chunks from cluster_start[0] on are
+ *   processed, against a cache of all n_tokens keys; earlier output rows are not written.
  * sel_cnt (device) receives min(k, n_cand) per cluster (also host-computable from the geometry).
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens / B]; candidate entries
  *   receive their score, every other entry -1.
@@ -136,8 +144,9 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
                                   const int32_t* sel_cnt, void* out);
 
 /* Anchor-based clustering of the sub-chunks of an outer chunk (Sec. 5.1.1-5.1.2, Algorithm 1,
- * Eq. 8), producing the cluster_start the calls above take. For every sub-chunk i (rows
- * [i L, min((i + 1) L, n_tokens)), M = ceil(n_tokens / L) of them) the fingerprint v_i is the mean
+ * Eq. 8), producing the cluster_start the calls above take, for the sub-chunks [first_subchunk, M),
+ * M = ceil(n_tokens / L) (first_subchunk > 0: the outer chunks of an incremental prefill that are
+ * still to run). For every sub-chunk i (rows [i L, min((i + 1) L, n_tokens))) the fingerprint v_i is the mean
  * of its query rows over all heads concatenated (Eq. 6, in R^(Hq d)). One left-to-right pass then
  * forms the clusters: a cluster opens at anchor a and admits the next sub-chunk j while
  * cos(v_a, v_j) >= theta and the cluster holds |C| sub-chunks with |C| * L < l_max; the first j
@@ -147,14 +156,17 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
  *   q             device bf16 [n_tokens][Hq][d], 0 < n_tokens <= max_tokens
  *   theta         similarity threshold (any value but NaN; > 1 gives single sub-chunks)
  *   l_max         cluster cap in tokens, >= 1 (the paper's default is 8 L)
- *   cluster_start HOST int32 with room for M + 1 entries: receives 0, ..., M
+ *   first_subchunk 0 <= first_subchunk < M
+ *   cluster_start HOST int32 with room for M - first_subchunk + 1 entries: receives first_subchunk, ..., M
  *   n_clusters    HOST: receives the number of clusters
- *   cos_band      optional HOST double [M][span]: cos(v_i, v_{i+o}) at [i][o - 1], NaN past the last
- *                 sub-chunk; span = min(ceil(l_max / L), outer_subchunks if > 0, M) - 1
+ *   cos_band      optional HOST double [M - first_subchunk][span]: cos(v_i, v_{i+o}) at
+ *                 [i - first_subchunk][o - 1], NaN past the last sub-chunk;
+ *                 span = min(ceil(l_max / L), outer_subchunks if > 0, M - first_subchunk) - 1
  * span above 64 returns SCALE_ERR_UNSUPPORTED. Synchronous: waits for the handle's stream. The
  * result does not count as a selection call. */
-scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, double theta,
-                                     int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
+scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens,
+                                     int32_t first_subchunk, double theta, int32_t l_max,
+                                     int32_t outer_subchunks, int32_t* cluster_start,
                                      int32_t* n_clusters, double* cos_band);
 
 /* Static text for a status code. Never NULL. */

@@ -53,6 +53,13 @@ their reasons in the design notes:
       too), so a cluster holds at most ceil(L_max / L) sub-chunks; clusters restart at each outer
       chunk boundary when the outer chunk length is given
   R24 the threshold test is taken in fp64
+  R25 incremental prefill (Sec. 3.1's outer-chunk loop): the clusters may cover only the last
+      sub-chunks [cluster_start[0], M); the cache holds every earlier token, and rows before
+      cluster_start[0] * L are not computed
+  R26 the overlap ratio (Eq. 7) compares the cluster's set I_C (anchor fingerprint, the cluster's
+      candidates) with the union of the sets each member sub-chunk selects on its own, as the
+      per-sub-chunk baseline would (its own fingerprint and its own candidate range, the
+      single-sub-chunk geometry); it is undefined (NaN) when I_C is empty
 """
 from __future__ import annotations
 
@@ -79,6 +86,7 @@ __all__ = [
     "subchunk_fingerprints",
     "normalized",
     "anchor_clustering",
+    "topk_overlap",
 ]
 
 
@@ -107,13 +115,14 @@ def geometry(n_tokens: int, sub_chunk: int, block_size: int, sink_tokens: int, l
     """Per-cluster geometry (Sec. 3.1 sub-chunks; Sec. 5.1.3 and Eq. 10 key groups; R9-R12).
 
     ``cluster_start`` holds sub-chunk indices: cluster j covers sub-chunks
-    [cluster_start[j], cluster_start[j+1]).
+    [cluster_start[j], cluster_start[j+1]). It may start past 0 (R25): incremental prefill of the
+    last outer chunks, whose keys follow those of the earlier, already prefilled ones in the cache.
     """
     L, B, S, W, k = sub_chunk, block_size, sink_tokens, local_window, top_k
     M = -(-n_tokens // L)
     cs = [int(x) for x in cluster_start]
-    if len(cs) < 2 or cs[0] != 0 or cs[-1] != M or any(b <= a for a, b in zip(cs, cs[1:])):
-        raise ValueError("cluster_start must rise strictly from 0 to ceil(n_tokens / sub_chunk)")
+    if len(cs) < 2 or cs[0] < 0 or cs[-1] != M or any(b <= a for a, b in zip(cs, cs[1:])):
+        raise ValueError("cluster_start must rise strictly to ceil(n_tokens / sub_chunk) from >= 0")
     out = []
     sink_blk = -(-S // B)
     for j in range(len(cs) - 1):
@@ -294,7 +303,7 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
         margins.append(margin)
     out = None
     if with_output:
-        out = np.empty((n_tokens, q.shape[1], q.shape[2]), dtype=np.float64)
+        out = np.full((n_tokens, q.shape[1], q.shape[2]), np.nan, dtype=np.float64)
         for j, g in enumerate(geo):
             sel = sels[j] if external_sel is None else np.asarray(external_sel[j], dtype=np.int64)
             out[g.s:g.e] = cluster_attention(q, k_pages, v_pages, block_table, g, sel, block_size,
@@ -333,19 +342,21 @@ def normalized(v) -> np.ndarray:
         return v / np.linalg.norm(v, axis=-1, keepdims=True)
 
 
-def anchor_clustering(vt, theta: float, sub_chunk: int, l_max: int, outer_subchunks: int = 0) -> np.ndarray:
+def anchor_clustering(vt, theta: float, sub_chunk: int, l_max: int, outer_subchunks: int = 0,
+                      first: int = 0) -> np.ndarray:
     """Algorithm 1 (Sec. 5.1.2): one left-to-right pass over the normalised fingerprints ``vt``.
 
     The open cluster starts at anchor a; sub-chunk j joins while cos(v_a, v_j) = vt[a] . vt[j]
     reaches ``theta`` and the cluster's current size |C| satisfies |C| * L < L_max (Eq. 8); the
     first j that fails either test closes the cluster and becomes the next anchor. With
     ``outer_subchunks`` > 0 the pass also closes a cluster at every outer-chunk boundary (R23).
-    Returns cluster_start as int32 [n_clusters + 1] in sub-chunk units (first 0, last M).
+    The pass starts at sub-chunk ``first`` (the outer chunks still to prefill, R25).
+    Returns cluster_start as int32 [n_clusters + 1] in sub-chunk units (first ``first``, last M).
     """
     vt = np.asarray(vt, dtype=np.float64)
     m = vt.shape[0]
     starts = []
-    a = 0
+    a = first
     while a < m:
         starts.append(a)
         end = m if outer_subchunks <= 0 else min(m, (a // outer_subchunks + 1) * outer_subchunks)
@@ -357,3 +368,18 @@ def anchor_clustering(vt, theta: float, sub_chunk: int, l_max: int, outer_subchu
         a = j
     starts.append(m)
     return np.asarray(starts, dtype=np.int32)
+
+
+def topk_overlap(cluster_sets, subchunk_sets, cluster_start) -> np.ndarray:
+    """Eq. 7 per cluster (R26): rho(C) = |I_C & U_j I_j| / |I_C|, with I_C the cluster's selection and
+    I_j the selections of its member sub-chunks j in [cluster_start[c], cluster_start[c + 1]) made
+    one sub-chunk at a time; ``subchunk_sets[j]`` is indexed by absolute sub-chunk. NaN when I_C is
+    empty."""
+    out = np.empty(len(cluster_sets), dtype=np.float64)
+    for c, i_c in enumerate(cluster_sets):
+        i_c = set(int(x) for x in i_c)
+        union = set()
+        for j in range(int(cluster_start[c]), int(cluster_start[c + 1])):
+            union |= set(int(x) for x in subchunk_sets[j])
+        out[c] = len(i_c & union) / len(i_c) if i_c else math.nan
+    return out

@@ -26,7 +26,7 @@ SCALE_OUT_BF16 = 1
 EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
-    "scale_stage_times", "scale_cluster_subchunks",
+    "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range",
 )
 STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster")
 
@@ -80,7 +80,9 @@ def _load():
     lib.scale_enable_timing.restype = ctypes.c_int
     lib.scale_stage_times.argtypes = [vp, vp, vp, ctypes.c_int]
     lib.scale_stage_times.restype = ctypes.c_int
-    lib.scale_cluster_subchunks.argtypes = [vp, vp, i32, ctypes.c_double, i32, i32, vp, vp, vp]
+    lib.scale_cluster_subchunks.argtypes = [vp, vp, i32, i32, ctypes.c_double, i32, i32, vp, vp, vp]
+    lib.scale_rep_keys_range.argtypes = [vp, vp, vp, i32, i32, vp]
+    lib.scale_rep_keys_range.restype = ctypes.c_int
     lib.scale_cluster_subchunks.restype = ctypes.c_int
     return lib
 
@@ -175,6 +177,10 @@ class Scale:
         _check(lib.scale_rep_keys(self._h, _ptr(k_pages), _ptr(block_table), int(n_tokens), _ptr(k_rep)),
                "scale_rep_keys")
 
+    def rep_keys_range(self, k_pages, block_table, first_block: int, n_tokens: int, k_rep):
+        _check(lib.scale_rep_keys_range(self._h, _ptr(k_pages), _ptr(block_table), int(first_block), int(n_tokens),
+                                        _ptr(k_rep)), "scale_rep_keys_range")
+
     def select_cluster(self, q, n_tokens: int, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None,
                        fingerprints_out=None):
         cs = _cluster_start(cluster_start)
@@ -190,18 +196,18 @@ class Scale:
                "scale_sparse_prefill")
 
     def cluster_subchunks(self, q, n_tokens: int, theta: float, l_max: int, outer_subchunks: int = 0,
-                          with_band: bool = False):
-        """Anchor-based clustering of the sub-chunks; returns cluster_start (int32 [n + 1]) and, with
-        ``with_band``, the cosine band [M][span] (see include/scale.h)."""
+                          with_band: bool = False, first_subchunk: int = 0):
+        """Anchor-based clustering of the sub-chunks [first_subchunk, M); returns cluster_start
+        (int32 [n + 1]) and, with ``with_band``, the cosine band [M - first][span] (include/scale.h)."""
         L = self.cfg.sub_chunk
-        m = -(-int(n_tokens) // L)
-        cs = np.zeros(m + 1, dtype=np.int32)
+        m = -(-int(n_tokens) // L) - int(first_subchunk)
+        cs = np.zeros(max(m, 0) + 1, dtype=np.int32)
         n = ctypes.c_int32()
         band = None
         if with_band:
-            band = np.full((m, cluster_span(l_max, L, outer_subchunks, m)), np.nan, dtype=np.float64)
-        _check(lib.scale_cluster_subchunks(self._h, _ptr(q), int(n_tokens), float(theta), int(l_max),
-                                           int(outer_subchunks), cs.ctypes.data, ctypes.byref(n),
+            band = np.full((max(m, 0), max(cluster_span(l_max, L, outer_subchunks, m), 0)), np.nan, dtype=np.float64)
+        _check(lib.scale_cluster_subchunks(self._h, _ptr(q), int(n_tokens), int(first_subchunk), float(theta),
+                                           int(l_max), int(outer_subchunks), cs.ctypes.data, ctypes.byref(n),
                                            None if band is None or band.size == 0 else band.ctypes.data),
                "scale_cluster_subchunks")
         cs = cs[:n.value + 1].copy()
@@ -249,8 +255,12 @@ def scale_retrieval_calls(h: Scale) -> int:
     return h.retrieval_calls()
 
 
-def scale_cluster_subchunks(h: Scale, q, n_tokens, theta, l_max, outer_subchunks=0, with_band=False):
-    return h.cluster_subchunks(q, n_tokens, theta, l_max, outer_subchunks, with_band)
+def scale_cluster_subchunks(h: Scale, q, n_tokens, first_subchunk, theta, l_max, outer_subchunks=0, with_band=False):
+    return h.cluster_subchunks(q, n_tokens, theta, l_max, outer_subchunks, with_band, first_subchunk)
+
+
+def scale_rep_keys_range(h: Scale, k_pages, block_table, first_block, n_tokens, k_rep):
+    h.rep_keys_range(k_pages, block_table, first_block, n_tokens, k_rep)
 
 
 def cluster_span(l_max: int, sub_chunk: int, outer_subchunks: int, m: int) -> int:

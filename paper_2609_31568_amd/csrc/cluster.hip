@@ -23,11 +23,12 @@ constexpr int kSumCols = 512;   // columns of the Hq*d row per work-group (64 la
 
 // grid: (column slice, sub-chunk). Lane l of wave w owns 8 columns and sums rows w, w + 8, ...
 __global__ __launch_bounds__(kSumThreads) void subchunk_sums(const uint16_t* __restrict__ q, int n_tokens,
-                                                             int sub_chunk, int row_elems, double* __restrict__ fp) {
+                                                             int first_subchunk, int sub_chunk, int row_elems,
+                                                             double* __restrict__ fp) {
   constexpr int kWaves = kSumThreads / 64;
   __shared__ double part[kWaves][kSumCols];
-  const int i = blockIdx.y;
-  const int r0 = i * sub_chunk;
+  const int i = blockIdx.y;                       // local index: sub-chunk first_subchunk + i
+  const int r0 = (first_subchunk + i) * sub_chunk;
   const int n_rows = min(sub_chunk, n_tokens - r0);
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int col = blockIdx.x * kSumCols + lane * 8;
@@ -100,14 +101,14 @@ __global__ __launch_bounds__(kThreads) void cos_band(const double* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int sub_chunk, int num_q_heads,
-                                      int head_dim, int span, double* fingerprints, double* inv_norm,
-                                      double* band, hipStream_t stream) {
-  const int m = (n_tokens + sub_chunk - 1) / sub_chunk;
+hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int first_subchunk, int sub_chunk,
+                                      int num_q_heads, int head_dim, int span, double* fingerprints,
+                                      double* inv_norm, double* band, hipStream_t stream) {
+  const int m = (n_tokens + sub_chunk - 1) / sub_chunk - first_subchunk;
   if (m <= 0) return hipSuccess;
   const int row_elems = num_q_heads * head_dim;
-  subchunk_sums<<<dim3((row_elems + kSumCols - 1) / kSumCols, m), kSumThreads, 0, stream>>>(q, n_tokens, sub_chunk,
-                                                                                           row_elems, fingerprints);
+  subchunk_sums<<<dim3((row_elems + kSumCols - 1) / kSumCols, m), kSumThreads, 0, stream>>>(
+      q, n_tokens, first_subchunk, sub_chunk, row_elems, fingerprints);
   inv_norms<<<m, kThreads, 0, stream>>>(fingerprints, row_elems, inv_norm);
   if (span > 0)
     cos_band<<<dim3(span, m), kThreads, 0, stream>>>(fingerprints, inv_norm, m, row_elems, span, band);

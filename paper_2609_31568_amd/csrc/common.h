@@ -30,8 +30,9 @@ static_assert(sizeof(WorkItem) == 16, "WorkItem is uploaded as raw bytes");
 
 // ---- launchers (each defined next to its kernel) ----
 
-// k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32).
-hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int n_blocks,
+// k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32), for the
+// logical blocks b in [first_block, n_blocks).
+hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int first_block, int n_blocks,
                            int num_kv_heads, int block_size, int head_dim, float* k_rep,
                            hipStream_t stream);
 
@@ -57,12 +58,12 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
                             int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                             hipStream_t stream);
 
-// Sub-chunk similarity for the anchor-based clustering: fp64 fingerprints [M][Hq * d] of every
-// sub-chunk, their inverse norms [M], and band[i][o - 1] = cos(v_i, v_{i+o}) for o = 1 .. span
-// (NaN past the last sub-chunk), M = ceil(n_tokens / sub_chunk).
-hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int sub_chunk, int num_q_heads,
-                                      int head_dim, int span, double* fingerprints, double* inv_norm,
-                                      double* band, hipStream_t stream);
+// Sub-chunk similarity for the anchor-based clustering of sub-chunks [first, M), M =
+// ceil(n_tokens / sub_chunk), indexed from first: fp64 fingerprints [M - first][Hq * d], their
+// inverse norms, and band[i][o - 1] = cos(v_i, v_{i+o}) for o = 1 .. span (NaN past the last).
+hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int first_subchunk, int sub_chunk,
+                                      int num_q_heads, int head_dim, int span, double* fingerprints,
+                                      double* inv_norm, double* band, hipStream_t stream);
 constexpr int kMaxClusterSpan = 64;   // largest band width (cluster cap - 1) the library supports
 
 // Block-sparse attention over the work list.

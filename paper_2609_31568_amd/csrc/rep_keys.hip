@@ -16,12 +16,13 @@ constexpr int kThreads = 256;
 template <int D, int B>
 __global__ __launch_bounds__(kThreads) void rep_keys_kernel(const uint16_t* __restrict__ k_pages,
                                                             const int32_t* __restrict__ block_table,
-                                                            int num_kv_heads, float* __restrict__ k_rep) {
+                                                            int first_block, int num_kv_heads,
+                                                            float* __restrict__ k_rep) {
   constexpr int kChunks = D / 8;                 // 16-byte chunks per row
   constexpr int kRowGroups = kThreads / kChunks; // rows handled in parallel
   constexpr int kRowsPerThread = B / kRowGroups; // all of a thread's loads are issued together
   static_assert(B % kRowGroups == 0, "whole rows per thread");
-  const int b = blockIdx.x / num_kv_heads;
+  const int b = first_block + (int)(blockIdx.x / num_kv_heads);
   const int g = blockIdx.x % num_kv_heads;
   const int page = block_table ? block_table[b] : b;
   const uint16_t* tile = k_pages + ((int64_t)page * num_kv_heads + g) * B * D;
@@ -58,19 +59,19 @@ __global__ __launch_bounds__(kThreads) void rep_keys_kernel(const uint16_t* __re
 
 }  // namespace
 
-hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int n_blocks,
+hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int first_block, int n_blocks,
                            int num_kv_heads, int block_size, int head_dim, float* k_rep,
                            hipStream_t stream) {
-  if (n_blocks <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((int64_t)n_blocks * num_kv_heads));
+  if (n_blocks <= first_block) return hipSuccess;
+  const dim3 grid((unsigned)((int64_t)(n_blocks - first_block) * num_kv_heads));
   if (head_dim == 128 && block_size == 128)
-    rep_keys_kernel<128, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+    rep_keys_kernel<128, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, first_block, num_kv_heads, k_rep);
   else if (head_dim == 128)
-    rep_keys_kernel<128, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+    rep_keys_kernel<128, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, first_block, num_kv_heads, k_rep);
   else if (block_size == 128)
-    rep_keys_kernel<64, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+    rep_keys_kernel<64, 128><<<grid, kThreads, 0, stream>>>(k_pages, block_table, first_block, num_kv_heads, k_rep);
   else
-    rep_keys_kernel<64, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, num_kv_heads, k_rep);
+    rep_keys_kernel<64, 64><<<grid, kThreads, 0, stream>>>(k_pages, block_table, first_block, num_kv_heads, k_rep);
   return hipGetLastError();
 }
 

@@ -98,7 +98,7 @@ scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens || n_clusters > c.max_clusters) return SCALE_ERR_CAPACITY;
   const int64_t M = ((int64_t)n_tokens + c.sub_chunk - 1) / c.sub_chunk;
-  if (cluster_start[0] != 0 || cluster_start[n_clusters] != M) return SCALE_ERR_INVALID_ARG;
+  if (cluster_start[0] < 0 || cluster_start[n_clusters] != M) return SCALE_ERR_INVALID_ARG;
   for (int j = 0; j < n_clusters; ++j)
     if (cluster_start[j + 1] <= cluster_start[j]) return SCALE_ERR_INVALID_ARG;
   if (!geo) return SCALE_OK;
@@ -303,8 +303,22 @@ scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
   stage_begin(h);
-  const hipError_t e = scale::launch_rep_keys(k_pages, block_table, n_tokens / c.block_size, c.num_kv_heads,
+  const hipError_t e = scale::launch_rep_keys(k_pages, block_table, 0, n_tokens / c.block_size, c.num_kv_heads,
                                               c.block_size, c.head_dim, k_rep, h->stream);
+  stage_end(h, SCALE_STAGE_REP_KEYS);
+  return check_launch(e);
+}
+
+scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const int32_t* block_table,
+                                  int32_t first_block, int32_t n_tokens, float* k_rep) {
+  if (!h || !k_pages || !k_rep || n_tokens < 1 || first_block < 0) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
+  if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
+  if (first_block > n_tokens / c.block_size) return SCALE_ERR_INVALID_ARG;
+  stage_begin(h);
+  const hipError_t e = scale::launch_rep_keys(k_pages, block_table, first_block, n_tokens / c.block_size,
+                                              c.num_kv_heads, c.block_size, c.head_dim, k_rep, h->stream);
   stage_end(h, SCALE_STAGE_REP_KEYS);
   return check_launch(e);
 }
@@ -357,21 +371,24 @@ static int32_t cluster_span(int32_t l_max, int32_t sub_chunk, int32_t outer_subc
   return (int32_t)(cap - 1);
 }
 
-scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, double theta,
-                                     int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
+scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, int32_t first_subchunk,
+                                     double theta, int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
                                      int32_t* n_clusters, double* cos_band) {
   if (!h || !q || !cluster_start || !n_clusters) return SCALE_ERR_INVALID_ARG;
   if (n_tokens < 1 || std::isnan(theta) || l_max < 1 || outer_subchunks < 0) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
   const int32_t L = c.sub_chunk;
-  const int32_t m = (n_tokens + L - 1) / L;
+  const int32_t M = (n_tokens + L - 1) / L;
+  if (first_subchunk < 0 || first_subchunk >= M) return SCALE_ERR_INVALID_ARG;
+  const int32_t m = M - first_subchunk;     // sub-chunks clustered; band rows are indexed from first
   const int32_t span = cluster_span(l_max, L, outer_subchunks, m);
   if (span > scale::kMaxClusterSpan) return SCALE_ERR_UNSUPPORTED;
 
   stage_begin(h);
-  scale_status st = check_launch(scale::launch_subchunk_similarity(q, n_tokens, L, c.num_q_heads, c.head_dim, span,
-                                                                   h->d_sub_fp, h->d_inv_norm, h->d_band, h->stream));
+  scale_status st = check_launch(scale::launch_subchunk_similarity(q, n_tokens, first_subchunk, L, c.num_q_heads,
+                                                                   c.head_dim, span, h->d_sub_fp, h->d_inv_norm,
+                                                                   h->d_band, h->stream));
   if (st == SCALE_OK && span > 0 &&
       hipMemcpyAsync(h->h_band, h->d_band, sizeof(double) * (size_t)m * span, hipMemcpyDeviceToHost, h->stream) !=
           hipSuccess)
@@ -385,19 +402,19 @@ scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t 
   // at an outer-chunk boundary. j - a - 1 < span always holds in the loop.
   const int64_t cap = ((int64_t)l_max + L - 1) / L;
   int32_t k = 0;
-  int32_t a = 0;
-  while (a < m) {
+  int32_t a = first_subchunk;
+  while (a < M) {
     cluster_start[k++] = a;
-    const int32_t end = outer_subchunks > 0 ? std::min(m, (a / outer_subchunks + 1) * outer_subchunks) : m;
+    const int32_t end = outer_subchunks > 0 ? std::min(M, (a / outer_subchunks + 1) * outer_subchunks) : M;
     int64_t size = 1;
     int32_t j = a + 1;
-    while (j < end && size < cap && h->h_band[(int64_t)a * span + (j - a - 1)] >= theta) {
+    while (j < end && size < cap && h->h_band[(int64_t)(a - first_subchunk) * span + (j - a - 1)] >= theta) {
       ++size;
       ++j;
     }
     a = j;
   }
-  cluster_start[k] = m;
+  cluster_start[k] = M;
   *n_clusters = k;
   if (cos_band && span > 0) std::memcpy(cos_band, h->h_band, sizeof(double) * (size_t)m * span);
   return SCALE_OK;

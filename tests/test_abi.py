@@ -90,7 +90,8 @@ def test_calls_reject_null_handle():
     assert lib.scale_retrieval_calls(None, ctypes.byref(n)) == -1
     out = np.zeros(4, dtype=np.int32)
     k = ctypes.c_int32()
-    assert lib.scale_cluster_subchunks(None, 1, 128, 0.95, 4096, 0, out.ctypes.data, ctypes.byref(k), None) == -1
+    assert lib.scale_cluster_subchunks(None, 1, 128, 0, 0.95, 4096, 0, out.ctypes.data, ctypes.byref(k), None) == -1
+    assert lib.scale_rep_keys_range(None, 1, None, 0, 128, 1) == -1
     lib.scale_free(None)        # no-op
 
 
@@ -135,9 +136,25 @@ def test_geometry_short_last_subchunk_and_odd_clusters():
     assert geo[-1][1] == n and geo[-1][0] == 9 * 256
 
 
+def test_geometry_of_a_suffix_of_clusters():
+    """Incremental prefill: clusters covering only the last sub-chunks have the geometry those
+    clusters have in the whole partition."""
+    pk = _pk()
+    cfg = _cfg(num_q_heads=4, num_kv_heads=1, head_dim=64, block_size=64, sub_chunk=256, top_k=4,
+               sink_tokens=64, local_window=300, max_tokens=8192, max_clusters=8)
+    full = np.array([0, 3, 4, 9, 12, 16, 20, 32], dtype=np.int32)
+    g_full = pk.scale_cluster_geometry(cfg, 8192, full)
+    for cut in (1, 3, 5):
+        g = pk.scale_cluster_geometry(cfg, 8192, full[cut:])
+        assert np.array_equal(g, g_full[cut:])
+        ref = oracle.geometry(8192, 256, 64, 64, 300, 4, full[cut:])
+        assert [tuple(int(x) for x in r) for r in g] == [(r.s, r.e, r.lo_blk, r.sink_eff, r.n_cand, r.sel_cnt)
+                                                       for r in ref]
+
+
 @pytest.mark.parametrize("cs,n,status", [
     ([0, 2, 2, 8], 2048, -1),        # not strictly increasing
-    ([1, 8], 2048, -1),              # does not start at 0
+    ([-1, 8], 2048, -1),             # starts below 0
     ([0, 7], 2048, -1),              # does not end at M
     ([0, 9], 2048, -1),
     ([0, 8], 2000, -2),              # n_tokens not a multiple of the block size

@@ -159,3 +159,24 @@ def test_generator_strength_draws_leave_topics_unchanged():
     assert np.all((lengths[:-1] >= 1) & (lengths[:-1] <= 5)) and 1 <= lengths[-1] <= 5
     assert all(len(set(t1[a:b].tolist())) == 1 for a, b in zip(cut[:-1], cut[1:]))
     assert np.array_equal(gen.q_rows(w, 0, 300), gen.q_rows(w.with_(q_scale_lo=2.0, q_scale_hi=2.0), 0, 300))
+
+
+def test_clustering_from_a_first_subchunk():
+    """Incremental clustering of the outer chunks still to run equals the tail of the whole pass
+    whenever the first sub-chunk starts an outer chunk."""
+    rng = np.random.default_rng(5)
+    vt = oracle.normalized(np.repeat(rng.normal(size=(6, 4)), 5, axis=0) + 0.05 * rng.normal(size=(30, 4)))
+    full = oracle.anchor_clustering(vt, 0.9, 512, 4096, outer_subchunks=10)
+    for first in (10, 20):
+        tail = oracle.anchor_clustering(vt, 0.9, 512, 4096, outer_subchunks=10, first=first)
+        assert tail[0] == first and tail[-1] == 30
+        assert np.array_equal(tail, full[np.searchsorted(full, first):])
+
+
+def test_topk_overlap_by_hand():
+    cs = [0, 3, 4]
+    cluster_sets = [[1, 2, 5, 9], [2]]
+    sub = [[1, 2], [7, 8], [5, 6], [3]]          # sub-chunk 3 alone forms cluster 1
+    rho = oracle.topk_overlap(cluster_sets, sub, cs)
+    assert rho[0] == 0.75 and rho[1] == 0.0
+    assert math.isnan(oracle.topk_overlap([[]], [[1]], [0, 1])[0])
