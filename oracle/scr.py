@@ -56,6 +56,9 @@ their reasons in the design notes:
   R25 incremental prefill (Sec. 3.1's outer-chunk loop): the clusters may cover only the last
       sub-chunks [cluster_start[0], M); the cache holds every earlier token, and rows before
       cluster_start[0] * L are not computed
+  R27 token-level selection (TokenSelect's granularity, Sec. 5.1.3): the candidates are the single
+      tokens between the sink blocks and the local window, each scored per head with its own key;
+      top_k counts tokens. Sinks and the local window keep their block rounding (R10, R11)
   R26 the overlap ratio (Eq. 7) compares the cluster's set I_C (anchor fingerprint, the cluster's
       candidates) with the union of the sets each member sub-chunk selects on its own, as the
       per-sub-chunk baseline would (its own fingerprint and its own candidate range, the
@@ -73,6 +76,8 @@ __all__ = [
     "geometry",
     "bf16_to_f64",
     "logical_kv",
+    "logical_rows",
+    "selected_positions",
     "rep_keys",
     "anchor_fingerprint",
     "block_logits",
@@ -106,12 +111,14 @@ class ClusterGeometry:
     lo_blk: int       # local window starts at token lo_blk * B
     sink_blk: int     # ceil(S / B): blocks reserved for the sink
     sink_eff: int     # sink blocks actually used: [0, sink_eff)
-    n_cand: int       # candidate blocks are [sink_blk, sink_blk + n_cand)
+    n_cand: int       # candidate blocks are [sink_blk, sink_blk + n_cand) (tokens: see below)
     sel_cnt: int      # min(k, n_cand)
+    tokens: bool = False   # token-level selection (R27): candidates are the TOKENS
+                           # [sink_blk * B, lo_blk * B), n_cand and sel_cnt count tokens
 
 
 def geometry(n_tokens: int, sub_chunk: int, block_size: int, sink_tokens: int, local_window: int,
-             top_k: int, cluster_start) -> list[ClusterGeometry]:
+             top_k: int, cluster_start, select_tokens: bool = False) -> list[ClusterGeometry]:
     """Per-cluster geometry (Sec. 3.1 sub-chunks; Sec. 5.1.3 and Eq. 10 key groups; R9-R12).
 
     ``cluster_start`` holds sub-chunk indices: cluster j covers sub-chunks
@@ -132,8 +139,9 @@ def geometry(n_tokens: int, sub_chunk: int, block_size: int, sink_tokens: int, l
         lo = max(0, min(s, e - W))
         lo_blk = lo // B
         sink_eff = min(sink_blk, lo_blk)
-        n_cand = max(0, lo_blk - sink_blk)
-        out.append(ClusterGeometry(s, e, anchor_end, lo_blk, sink_blk, sink_eff, n_cand, min(k, n_cand)))
+        n_cand = max(0, lo_blk - sink_blk) * (B if select_tokens else 1)
+        out.append(ClusterGeometry(s, e, anchor_end, lo_blk, sink_blk, sink_eff, n_cand, min(k, n_cand),
+                                   bool(select_tokens)))
     return out
 
 
@@ -154,6 +162,15 @@ def logical_kv(pages, block_table, blocks) -> np.ndarray:
     phys = np.asarray(block_table)[blocks]
     x = bf16_to_f64(pages[phys])                   # [nb, Hkv, B, d]
     return x.transpose(0, 2, 1, 3).reshape(-1, pages.shape[1], pages.shape[3])
+
+
+def logical_rows(pages, block_table, positions, block_size: int) -> np.ndarray:
+    """Keys (or values) at the given token positions as float64 [len(positions), Hkv, d]."""
+    positions = np.asarray(positions, dtype=np.int64)
+    if positions.size == 0:
+        return np.zeros((0, pages.shape[1], pages.shape[3]), dtype=np.float64)
+    phys = np.asarray(block_table)[positions // block_size]
+    return bf16_to_f64(pages[phys, :, positions % block_size, :])
 
 
 def rep_keys(k_pages, block_table, n_tokens: int, block_size: int, blocks=None) -> np.ndarray:
@@ -216,14 +233,22 @@ def select_topk(scores, first_block: int, k: int):
     return sel.astype(np.int64), margin
 
 
+def selected_positions(geo: ClusterGeometry, sel, block_size: int) -> np.ndarray:
+    """Token positions of the selected set: every token of each selected block, or the selected
+    tokens themselves (R27)."""
+    sel = np.asarray(sel, dtype=np.int64)
+    if geo.tokens:
+        return sel
+    return (sel[:, None] * block_size + np.arange(block_size)[None, :]).reshape(-1)
+
+
 def key_positions(geo: ClusterGeometry, sel, p: int, block_size: int) -> np.ndarray:
-    """Eq. 10 key set of query row p: sink blocks, the shared selected blocks, and the local
+    """Eq. 10 key set of query row p: sink blocks, the shared selected set, and the local
     window [lo_blk * B, p] (causal, R13). The three groups are disjoint by construction (R9)."""
     B = block_size
     sink = np.arange(0, geo.sink_eff * B)
-    chosen = (np.asarray(sel, dtype=np.int64)[:, None] * B + np.arange(B)[None, :]).reshape(-1)
     local = np.arange(geo.lo_blk * B, p + 1)
-    return np.concatenate([sink, chosen, local])
+    return np.concatenate([sink, selected_positions(geo, sel, B), local])
 
 
 def attention_rows(q, k_pages, v_pages, block_table, geo: ClusterGeometry, sel, rows, block_size: int,
@@ -244,16 +269,16 @@ def attention_rows(q, k_pages, v_pages, block_table, geo: ClusterGeometry, sel, 
     out = np.empty((len(rows), len(heads), d), dtype=np.float64)
     if len(rows) == 0:
         return out
-    # Logical keys/values of every block any requested row can see.
+    # Logical keys/values of every position any requested row can see: the sink and selected
+    # sets (visible to every row) then the local window up to the last requested row.
     p_max = int(rows.max())
-    blocks = np.concatenate([np.arange(geo.sink_eff), np.asarray(sel, dtype=np.int64),
-                             np.arange(geo.lo_blk, p_max // B + 1)]).astype(np.int64)
-    Kx = logical_kv(k_pages, block_table, blocks)        # [nk, Hkv, d]
-    Vx = logical_kv(v_pages, block_table, blocks)
-    pos = (blocks[:, None] * B + np.arange(B)[None, :]).reshape(-1)
+    fixed = np.concatenate([np.arange(geo.sink_eff * B), selected_positions(geo, sel, B)])
+    pos = np.concatenate([fixed, np.arange(geo.lo_blk * B, p_max + 1)]).astype(np.int64)
+    Kx = logical_rows(k_pages, block_table, pos, B)      # [nk, Hkv, d]
+    Vx = logical_rows(v_pages, block_table, pos, B)
     qx = bf16_to_f64(q[rows])                            # [nr, Hq, d]
     # Mask from the key-set definition: key t is visible to row p iff t is in Kset(p).
-    n_fixed = (geo.sink_eff + len(sel)) * B
+    n_fixed = len(fixed)
     visible = np.ones((len(rows), len(pos)), dtype=bool)
     visible[:, n_fixed:] = pos[None, n_fixed:] <= rows[:, None]
     for hi, h in enumerate(heads):
@@ -279,7 +304,8 @@ def cluster_attention(q, k_pages, v_pages, block_table, geo, sel, block_size, so
 
 def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, block_size: int,
             top_k: int, sink_tokens: int, local_window: int, cluster_start, score_scale: float = 1.0,
-            softmax_scale: float | None = None, with_output: bool = True, external_sel=None) -> dict:
+            softmax_scale: float | None = None, with_output: bool = True, external_sel=None,
+            select_tokens: bool = False) -> dict:
     """Algorithm 2 for one layer with a given cluster assignment.
 
     For each cluster: anchor fingerprint -> block logits -> soft-voting scores -> top-k
@@ -288,15 +314,24 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
     step, so attention can be checked under another selection.
     Returns a dict with geometry, k_rep, fingerprints, scores, selections, margins, output.
     """
-    geo = geometry(n_tokens, sub_chunk, block_size, sink_tokens, local_window, top_k, cluster_start)
+    geo = geometry(n_tokens, sub_chunk, block_size, sink_tokens, local_window, top_k, cluster_start,
+                   select_tokens)
     k_rep = rep_keys(k_pages, block_table, n_tokens, block_size)
     Hkv = k_pages.shape[1]
+    B = block_size
     fps, scores, sels, margins = [], [], [], []
     for g in geo:
         v = anchor_fingerprint(q, g.s, g.anchor_end)
-        x = block_logits(v, k_rep[g.sink_blk:g.sink_blk + g.n_cand], Hkv, score_scale)
+        if select_tokens:
+            # R27: the candidates are single tokens, scored with their own keys
+            cand = logical_rows(k_pages, block_table, np.arange(g.sink_blk * B, g.sink_blk * B + g.n_cand), B)
+            first = g.sink_blk * B
+        else:
+            cand = k_rep[g.sink_blk:g.sink_blk + g.n_cand]
+            first = g.sink_blk
+        x = block_logits(v, cand, Hkv, score_scale)
         sc = soft_vote(x)
-        sel, margin = select_topk(sc, g.sink_blk, top_k)
+        sel, margin = select_topk(sc, first, top_k)
         fps.append(v)
         scores.append(sc)
         sels.append(sel)

@@ -137,3 +137,46 @@ def brute_prefill(q_bits, k_pages, v_pages, block_table, n_tokens, L, B, S, W, k
     vis = visibility_mask(n_tokens, layout, sels, B)
     return {"layout": layout, "scores": scores, "selections": sels, "mask": vis,
             "output": masked_attention(q, K, V, vis)}
+
+
+def brute_prefill_tokens(q_bits, k_pages, v_pages, block_table, n_tokens, L, B, S, W, k, cluster_start,
+                         score_scale=1.0):
+    """Token-level selection by explicit loops: every single token between the sink blocks and the
+    local window is a candidate scored with its own key; exhaustive best-total k-subset; explicit
+    mask; dense masked softmax."""
+    q = widen(q_bits)
+    K = unpage(k_pages, block_table)
+    V = unpage(v_pages, block_table)
+    Hkv = k_pages.shape[1]
+    Hq = q.shape[1]
+    G = Hq // Hkv
+    layout = cluster_layout(n_tokens, L, B, S, W, cluster_start)
+    sels, scores = [], []
+    for (s, e, a_end, lo_blk, sink_eff, cand_blocks) in layout:
+        cand = [t for b in cand_blocks for t in range(b * B, (b + 1) * B)]
+        total = {t: 0.0 for t in cand}
+        for h in range(Hq):
+            g = h // G
+            logits = {}
+            for t in cand:
+                acc = 0.0
+                for p in range(s, a_end):
+                    acc += float(np.dot(K[t, g, :], q[p, h, :]))
+                logits[t] = score_scale * acc / (a_end - s)
+            if not logits:
+                continue
+            mx = max(logits.values())
+            den = sum(math.exp(x - mx) for x in logits.values())
+            for t in cand:
+                total[t] += math.exp(logits[t] - mx) / den
+        scores.append(total)
+        sels.append(brute_select(total, k))
+    vis = np.zeros((n_tokens, n_tokens), dtype=bool)
+    for (s, e, _a, lo_blk, sink_eff, _c), sel in zip(layout, sels):
+        allowed = set(range(sink_eff * B)) | set(sel)
+        for p in range(s, e):
+            for t in allowed | set(range(lo_blk * B, p + 1)):
+                assert t <= p, "a key after its query would be visible"
+                vis[p, t] = True
+    return {"layout": layout, "scores": scores, "selections": sels, "mask": vis,
+            "output": masked_attention(q, K, V, vis)}
