@@ -13,6 +13,10 @@
  *   scale_sparse_prefill  block-sparse attention of every query row over sink blocks, the
  *                         cluster's selected blocks and the causal local window
  *
+ * and, on a handle created with select_tokens = 1, its token-level form (the paper's own
+ * granularity): scale_select_cluster_tokens scores every single candidate token with its own key,
+ * top_k counts tokens, and scale_sparse_prefill attends over the selected tokens.
+ *
  * Conventions shared by every call:
  *  - Plain C; no HIP or framework types. bf16 tensors are passed as uint16_t bit patterns.
  *  - Device pointers are caller-owned device allocations (any HIP allocation visible to the
@@ -46,6 +50,9 @@
  *    sel_cnt  = min(k, n_cand)
  *    keys of row p in [s, e): sink blocks U selected blocks U tokens [lo_blk * B, p]
  * The three key groups are disjoint and every key lies at or before its query (causal).
+ * Token-level selection (select_tokens = 1): the candidates are the tokens
+ * [sink_blk * B, lo_blk * B) (n_cand = B * max(0, lo_blk - sink_blk)), sel_cnt = min(k, n_cand),
+ * the selected set is sel_cnt single tokens, and sinks and the local window keep their block form.
  */
 #ifndef SCALE_H_
 #define SCALE_H_
@@ -75,7 +82,8 @@ typedef struct {
   int32_t head_dim;      /* d: 64 or 128                                                     */
   int32_t block_size;    /* B: 64 or 128 tokens per KV block / page                          */
   int32_t sub_chunk;     /* L: query rows per sub-chunk, a positive multiple of B            */
-  int32_t top_k;         /* k >= 0 blocks selected per cluster (any size; sel_idx rows hold k) */
+  int32_t top_k;         /* k >= 0 blocks (tokens if select_tokens) selected per cluster;
+                            sel_idx rows hold k entries                                      */
   int32_t sink_tokens;   /* S >= 0: attention-sink tokens, rounded up to whole blocks        */
   int32_t local_window;  /* W >= 0: base local window in tokens                              */
   int32_t max_tokens;    /* capacity: largest n_tokens any call will pass (sizes scratch)    */
@@ -83,6 +91,8 @@ typedef struct {
   float softmax_scale;   /* attention logit scale; 0 means 1/sqrt(head_dim) (Eqs. 1, 10)     */
   float score_scale;     /* selection logit scale sigma; 0 means 1.0 (the literal v . k)     */
   int32_t out_dtype;     /* scale_out_dtype of the attention output                          */
+  int32_t select_tokens; /* 0: block-level selection; 1: token-level selection (top_k counts
+                            tokens; scale_init also allocates the token calls' scratch)      */
 } scale_config;
 
 /* Create a handle bound to the current HIP device and to `hip_stream` (a hipStream_t; NULL is
@@ -124,11 +134,32 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens / B]; candidate entries
  *   receive their score, every other entry -1.
  * fingerprints_out (optional, may be NULL): device fp32 [n_clusters][Hq][d] anchor fingerprints.
- * Each call adds n_clusters to the handle's retrieval-call counter. */
+ * Each call adds n_clusters to the handle's retrieval-call counter. On a select_tokens handle
+ * this call returns SCALE_ERR_UNSUPPORTED (use scale_select_cluster_tokens). */
 scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens,
                                   const float* k_rep, const int32_t* cluster_start,
                                   int32_t n_clusters, int32_t* sel_idx, int32_t* sel_cnt,
                                   float* scores_out, float* fingerprints_out);
+
+/* Token-level cluster selection (Eq. 9 with head soft-voting, Sec. 5.1.3, at the granularity of
+ * single tokens); handles created with select_tokens = 1 only (else SCALE_ERR_UNSUPPORTED):
+ *   v[h]     = mean of q[p][h] over the anchor rows
+ *   x[h][t]  = score_scale * v[h] . K[t][g(h)]    for candidate tokens t (their own keys, read
+ *              from k_pages through block_table)
+ *   score[t] = sum over h of softmax over candidates of x[h][.]   evaluated at t
+ *   sel      = top sel_cnt candidates by (score descending, token position ascending), emitted
+ *              in ascending order into sel_idx[j][0..sel_cnt), the rest of the row -1.
+ * The logits are computed on the matrix cores from a two-piece bf16 split of the fp32
+ * fingerprint (relative representation error <= 2^-18) with fp32 accumulation.
+ * cluster_start, sel_cnt and fingerprints_out as for scale_select_cluster.
+ * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens]; candidate entries
+ *   receive their score, every other entry -1.
+ * Each call adds n_clusters to the handle's retrieval-call counter. */
+scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens,
+                                         const uint16_t* k_pages, const int32_t* block_table,
+                                         const int32_t* cluster_start, int32_t n_clusters,
+                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                         float* fingerprints_out);
 
 /* Block-sparse prefill attention (Eq. 10): for every row p of every cluster and every query
  * head h, out[p][h] = softmax over Kset(p) of (q[p][h] . k_t * softmax_scale) weighted sum of
@@ -136,7 +167,10 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
  * sel_idx / sel_cnt are device arrays as written by scale_select_cluster (any ascending or
  * unordered set of distinct candidate blocks is accepted; entries are not re-validated on the
  * device beyond clamping sel_cnt to [0, top_k]). cluster_start is the same host array as for
- * the selection. bf16 output is the round-to-nearest-even of the fp32 result. */
+ * the selection. bf16 output is the round-to-nearest-even of the fp32 result.
+ * On a select_tokens handle, sel_idx rows hold token positions (as scale_select_cluster_tokens
+ * writes them; each is clamped to [0, n_tokens)) and Kset(p) = sink blocks U those tokens U tokens
+ * [lo_blk * B, p]; the selected keys and values are first gathered into handle scratch. */
 scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint16_t* k_pages,
                                   const uint16_t* v_pages, const int32_t* block_table,
                                   int32_t n_tokens, const int32_t* cluster_start,
@@ -183,7 +217,8 @@ typedef enum {
   SCALE_STAGE_VOTE_TOPK = 3,    /* soft-voting scores and top-k                          */
   SCALE_STAGE_ATTENTION = 4,    /* block-sparse attention                                */
   SCALE_STAGE_CLUSTER = 5,      /* sub-chunk similarity of scale_cluster_subchunks        */
-  SCALE_NUM_STAGES = 6
+  SCALE_STAGE_GATHER = 6,       /* gather of the selected tokens' keys and values          */
+  SCALE_NUM_STAGES = 7
 } scale_stage;
 
 /* Device-time instrumentation (off by default). While enabled, every stage's kernels of every
@@ -198,7 +233,8 @@ scale_status scale_stage_times(scale_handle h, double* ms, int64_t* launches, in
 
 /* Host-only geometry of each cluster, exactly as the calls above use it (no HIP call; usable
  * without a device). For cluster j, writes geo[j*6 + 0..5] =
- *   { s, e, lo_blk, sink_eff, n_cand, sel_cnt }.
+ *   { s, e, lo_blk, sink_eff, n_cand, sel_cnt }  (n_cand and sel_cnt in tokens on a
+ *   select_tokens config).
  * Same validation of cfg and cluster_start as the calls above. */
 scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens,
                                     const int32_t* cluster_start, int32_t n_clusters,

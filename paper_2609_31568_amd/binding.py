@@ -26,9 +26,9 @@ SCALE_OUT_BF16 = 1
 EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
-    "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range",
+    "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range", "scale_select_cluster_tokens",
 )
-STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster")
+STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster", "gather")
 
 
 class ScaleError(RuntimeError):
@@ -52,6 +52,7 @@ class scale_config(ctypes.Structure):
         ("softmax_scale", ctypes.c_float),
         ("score_scale", ctypes.c_float),
         ("out_dtype", ctypes.c_int32),
+        ("select_tokens", ctypes.c_int32),
     ]
 
 
@@ -68,6 +69,8 @@ def _load():
     lib.scale_rep_keys.restype = ctypes.c_int
     lib.scale_select_cluster.argtypes = [vp, vp, i32, vp, vp, i32, vp, vp, vp, vp]
     lib.scale_select_cluster.restype = ctypes.c_int
+    lib.scale_select_cluster_tokens.argtypes = [vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.scale_select_cluster_tokens.restype = ctypes.c_int
     lib.scale_sparse_prefill.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp]
     lib.scale_sparse_prefill.restype = ctypes.c_int
     lib.scale_status_string.argtypes = [ctypes.c_int]
@@ -117,9 +120,10 @@ def _cluster_start(cs) -> np.ndarray:
 
 def make_config(*, num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
                 local_window, max_tokens, max_clusters, softmax_scale=0.0, score_scale=0.0,
-                out_dtype=SCALE_OUT_F32) -> scale_config:
+                out_dtype=SCALE_OUT_F32, select_tokens=False) -> scale_config:
     return scale_config(num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
-                        local_window, max_tokens, max_clusters, softmax_scale, score_scale, out_dtype)
+                        local_window, max_tokens, max_clusters, softmax_scale, score_scale, out_dtype,
+                        1 if select_tokens else 0)
 
 
 def scale_cluster_geometry(cfg: scale_config, n_tokens: int, cluster_start) -> np.ndarray:
@@ -188,6 +192,14 @@ class Scale:
                                         _ptr(sel_idx), _ptr(sel_cnt), _ptr(scores_out), _ptr(fingerprints_out)),
                "scale_select_cluster")
 
+    def select_cluster_tokens(self, q, n_tokens: int, k_pages, block_table, cluster_start, sel_idx, sel_cnt,
+                              scores_out=None, fingerprints_out=None):
+        cs = _cluster_start(cluster_start)
+        _check(lib.scale_select_cluster_tokens(self._h, _ptr(q), int(n_tokens), _ptr(k_pages), _ptr(block_table),
+                                               cs.ctypes.data, len(cs) - 1, _ptr(sel_idx), _ptr(sel_cnt),
+                                               _ptr(scores_out), _ptr(fingerprints_out)),
+               "scale_select_cluster_tokens")
+
     def sparse_prefill(self, q, k_pages, v_pages, block_table, n_tokens: int, cluster_start, sel_idx, sel_cnt, out):
         cs = _cluster_start(cluster_start)
         _check(lib.scale_sparse_prefill(self._h, _ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(block_table),
@@ -245,6 +257,12 @@ def scale_rep_keys(h: Scale, k_pages, block_table, n_tokens, k_rep):
 def scale_select_cluster(h: Scale, q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None,
                          fingerprints_out=None):
     h.select_cluster(q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out, fingerprints_out)
+
+
+def scale_select_cluster_tokens(h: Scale, q, n_tokens, k_pages, block_table, cluster_start, sel_idx, sel_cnt,
+                                scores_out=None, fingerprints_out=None):
+    h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cluster_start, sel_idx, sel_cnt, scores_out,
+                            fingerprints_out)
 
 
 def scale_sparse_prefill(h: Scale, q, k_pages, v_pages, block_table, n_tokens, cluster_start, sel_idx, sel_cnt, out):

@@ -66,13 +66,52 @@ hipError_t launch_subchunk_similarity(const uint16_t* q, int n_tokens, int first
                                       double* inv_norm, double* band, hipStream_t stream);
 constexpr int kMaxClusterSpan = 64;   // largest band width (cluster cap - 1) the library supports
 
-// Block-sparse attention over the work list.
+// ---- token-level selection ----
+// Layout plan of the token scoring kernels for one call: fingerprint rows are (cluster, head of the
+// group) with the group padded to gp = a power of two; r_pad rows per KV head in groups of 128;
+// candidates in chunks of chunk_tokens (= tiles_per_chunk 64-token tiles), n_chunks of them.
+constexpr int kMaxTokenChunks = 256;
+constexpr int kTokenTile = 64;        // rows per gathered tile of selected tokens
+struct TokenPlan {
+  int gp, r_pad, n_rowgroups, tiles_per_chunk, n_chunks, chunk_tokens;
+};
+int token_group_pad(int group);
+int token_row_pad(int n_clusters, int group);
+TokenPlan plan_token_selection(int n_clusters, int group, int num_kv_heads, int max_cand);
+
+// Per-KV-head partial soft-voting scores of every candidate token: partial[j][g][c] = sum over the
+// query heads h of g of softmax_c(x[j][h][.]) at c, x = sigma * v[j][h] . K[first_token + c][g].
+// Scratch: F [Hkv][r_pad][2][d] bf16, stats [Hkv][r_pad][n_chunks], lse2 [Hkv][r_pad].
+hipError_t launch_token_selection(const float* fingerprints, const uint16_t* k_pages, const int32_t* block_table,
+                                  const ClusterGeo* geo, int n_clusters, int max_cand, int first_token,
+                                  int num_q_heads, int num_kv_heads, int head_dim, int block_size,
+                                  float score_scale, int64_t cand_stride, uint16_t* F, float2* stats, float* lse2,
+                                  float* partial, hipStream_t stream);
+
+// Score = sum of the partials over KV heads, then the deterministic top-k of vote_topk; entries are
+// token positions first_token + c. scores_out (optional) rows have n_tokens entries.
+hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
+                                   int first_token, int num_kv_heads, int top_k, int n_tokens, float* spill,
+                                   int32_t* sel_idx, int32_t* sel_cnt, float* scores_out, hipStream_t stream);
+
+// Selected keys and values of every cluster copied to gk / gv [cluster][Hkv][kpad][d] in selection
+// order, kpad = top_k rounded up to kTokenTile; the rows of the last partial tile past sel_cnt are
+// zero.
+hipError_t launch_gather_selected(const uint16_t* k_pages, const uint16_t* v_pages, const int32_t* block_table,
+                                  const int32_t* sel_idx, const int32_t* sel_cnt, int n_clusters, int top_k,
+                                  int kpad, int n_tokens, int num_kv_heads, int head_dim, int block_size,
+                                  uint16_t* gk, uint16_t* gv, hipStream_t stream);
+
+// Block-sparse attention over the work list. With gk != null (token-level selection) the selected
+// keys are the gathered rows gk / gv [cluster][Hkv][kpad][d], sel_cnt[j] of them, instead of the
+// blocks sel_idx names.
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
                                    const WorkItem* items, int n_items, const int32_t* sel_idx,
                                    const int32_t* sel_cnt, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
-                                   float qk_scale_log2, int out_bf16, void* out, hipStream_t stream);
+                                   float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
+                                   const uint16_t* gv, int kpad, hipStream_t stream);
 
 // Query positions per attention work item for a group of `group` query heads per KV head
 // (a multiple of kTilePositions), and the number of head groups one KV head's query heads are

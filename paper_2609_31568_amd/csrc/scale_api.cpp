@@ -58,6 +58,16 @@ struct scale_ctx {
   double* d_inv_norm = nullptr;
   double* d_band = nullptr;
   double* h_band = nullptr;
+  // token-level selection (select_tokens): fingerprint pieces, chunk statistics, log-normalisers,
+  // per-KV-head partial scores, the score rows of the top-k, and the gathered keys / values
+  int kpad = 0;              // top_k rounded up to a whole gathered tile
+  uint16_t* d_tok_F = nullptr;
+  float2* d_tok_stats = nullptr;
+  float* d_tok_lse = nullptr;
+  float* d_tok_partial = nullptr;
+  float* d_tok_score = nullptr;
+  uint16_t* d_gk = nullptr;
+  uint16_t* d_gv = nullptr;
   // pinned staging ring
   size_t slot_bytes = 0;
   Slot slots[kRingSlots];
@@ -82,12 +92,19 @@ scale_status validate_config(const scale_config* c) {
   if (!std::isfinite(c->softmax_scale) || c->softmax_scale < 0.f) return SCALE_ERR_INVALID_ARG;
   if (!std::isfinite(c->score_scale)) return SCALE_ERR_INVALID_ARG;
   if (c->out_dtype != SCALE_OUT_F32 && c->out_dtype != SCALE_OUT_BF16) return SCALE_ERR_INVALID_ARG;
+  if (c->select_tokens != 0 && c->select_tokens != 1) return SCALE_ERR_INVALID_ARG;
   if (c->head_dim != 64 && c->head_dim != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->block_size != 64 && c->block_size != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->sub_chunk % c->block_size) return SCALE_ERR_UNSUPPORTED;
   if (c->num_q_heads / c->num_kv_heads > 8) return SCALE_ERR_UNSUPPORTED;
   // sizes that keep every int32 index of the kernels in range
   if ((int64_t)c->max_tokens * c->num_q_heads * c->head_dim >= ((int64_t)1 << 40)) return SCALE_ERR_UNSUPPORTED;
+  if (c->select_tokens) {
+    // gathered rows and token-scoring rows are int32 indices in the kernels
+    const int64_t kpad = ((int64_t)c->top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
+    if ((int64_t)c->max_clusters * c->num_kv_heads * kpad >= ((int64_t)1 << 31)) return SCALE_ERR_UNSUPPORTED;
+    if ((int64_t)c->max_clusters * 8 * c->num_kv_heads >= ((int64_t)1 << 24)) return SCALE_ERR_UNSUPPORTED;
+  }
   return SCALE_OK;
 }
 
@@ -112,7 +129,7 @@ scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_
     const int lo = std::max(0, std::min(g.s, g.e - c.local_window));
     g.lo_blk = lo / B;
     g.sink_eff = std::min(sink_blk, g.lo_blk);
-    g.n_cand = std::max(0, g.lo_blk - sink_blk);
+    g.n_cand = std::max(0, g.lo_blk - sink_blk) * (c.select_tokens ? B : 1);
     g.sel_cnt = std::min(c.top_k, g.n_cand);
     g.pad = 0;
   }
@@ -174,6 +191,13 @@ void release(scale_ctx* h) {
   (void)hipFree(h->d_inv_norm);
   (void)hipFree(h->d_band);
   if (h->h_band) (void)hipHostFree(h->h_band);
+  (void)hipFree(h->d_tok_F);
+  (void)hipFree(h->d_tok_stats);
+  (void)hipFree(h->d_tok_lse);
+  (void)hipFree(h->d_tok_partial);
+  (void)hipFree(h->d_tok_score);
+  (void)hipFree(h->d_gk);
+  (void)hipFree(h->d_gv);
   delete h;
 }
 
@@ -266,6 +290,18 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
             dev((void**)&h->d_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan) &&
             hipHostMalloc((void**)&h->h_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan,
                           hipHostMallocDefault) == hipSuccess;
+  if (ok && c.select_tokens) {
+    const int group = c.num_q_heads / c.num_kv_heads;
+    const int64_t rows = (int64_t)c.num_kv_heads * scale::token_row_pad(c.max_clusters, group);
+    h->kpad = (c.top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
+    const int64_t gathered = mc * c.num_kv_heads * h->kpad * c.head_dim;
+    ok = dev((void**)&h->d_tok_F, sizeof(uint16_t) * rows * 2 * c.head_dim) &&
+         dev((void**)&h->d_tok_stats, sizeof(float2) * rows * scale::kMaxTokenChunks) &&
+         dev((void**)&h->d_tok_lse, sizeof(float) * rows) &&
+         dev((void**)&h->d_tok_partial, sizeof(float) * mc * c.num_kv_heads * (int64_t)c.max_tokens) &&
+         dev((void**)&h->d_tok_score, sizeof(float) * mc * (int64_t)c.max_tokens) &&
+         dev((void**)&h->d_gk, sizeof(uint16_t) * gathered) && dev((void**)&h->d_gv, sizeof(uint16_t) * gathered);
+  }
   if (!ok) {
     (void)hipGetLastError();
     release(h);
@@ -328,6 +364,7 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
                                   int32_t* sel_cnt, float* scores_out, float* fingerprints_out) {
   if (!h || !q || !k_rep || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
+  if (c.select_tokens) return SCALE_ERR_UNSUPPORTED;
   scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
@@ -357,6 +394,48 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
   st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_head_stats, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
                                             c.num_q_heads, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
                                             scores_out, h->stream));
+  stage_end(h, SCALE_STAGE_VOTE_TOPK);
+  if (st != SCALE_OK) return st;
+  h->retrieval_calls += n_clusters;
+  return SCALE_OK;
+}
+
+scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens, const uint16_t* k_pages,
+                                         const int32_t* block_table, const int32_t* cluster_start, int32_t n_clusters,
+                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                         float* fingerprints_out) {
+  if (!h || !q || !k_pages || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
+  const scale_config& c = h->cfg;
+  if (!c.select_tokens) return SCALE_ERR_UNSUPPORTED;
+  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  if (st != SCALE_OK) return st;
+
+  Slot* slot = nullptr;
+  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
+  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  int max_cand = 0;
+  for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
+  if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
+
+  const int first_token = (c.sink_tokens + c.block_size - 1) / c.block_size * c.block_size;
+  const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
+  float* fps = fingerprints_out ? fingerprints_out : h->d_fingerprints;
+  stage_begin(h);
+  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, h->stream));
+  stage_end(h, SCALE_STAGE_FINGERPRINT);
+  if (st != SCALE_OK) return st;
+  stage_begin(h);
+  st = check_launch(scale::launch_token_selection(fps, k_pages, block_table, h->d_geo, n_clusters, max_cand,
+                                                  first_token, c.num_q_heads, c.num_kv_heads, c.head_dim,
+                                                  c.block_size, sigma, c.max_tokens, h->d_tok_F, h->d_tok_stats,
+                                                  h->d_tok_lse, h->d_tok_partial, h->stream));
+  stage_end(h, SCALE_STAGE_LOGITS);
+  if (st != SCALE_OK) return st;
+  stage_begin(h);
+  st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, c.max_tokens, first_token,
+                                                   c.num_kv_heads, c.top_k, n_tokens, h->d_tok_score, sel_idx,
+                                                   sel_cnt, scores_out, h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
   h->retrieval_calls += n_clusters;
@@ -468,11 +547,20 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
 
   const float scale = c.softmax_scale == 0.f ? 1.0f / std::sqrt((float)c.head_dim) : c.softmax_scale;
   const float qk_scale_log2 = scale * 1.4426950408889634f;
+  const bool tokens = c.select_tokens && h->kpad > 0;
+  if (tokens) {
+    stage_begin(h);
+    st = check_launch(scale::launch_gather_selected(k_pages, v_pages, block_table, sel_idx, sel_cnt, n_clusters,
+                                                    c.top_k, h->kpad, n_tokens, c.num_kv_heads, c.head_dim, B,
+                                                    h->d_gk, h->d_gv, h->stream));
+    stage_end(h, SCALE_STAGE_GATHER);
+    if (st != SCALE_OK) return st;
+  }
   stage_begin(h);
-  const hipError_t e = scale::launch_sparse_attention(q, k_pages, v_pages, block_table, h->d_geo, h->d_items,
-                                                      (int)n_items, sel_idx, sel_cnt, c.top_k, c.num_q_heads,
-                                                      c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
-                                                      c.out_dtype == SCALE_OUT_BF16, out, h->stream);
+  const hipError_t e = scale::launch_sparse_attention(
+      q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, c.top_k,
+      c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2, c.out_dtype == SCALE_OUT_BF16, out,
+      tokens ? h->d_gk : nullptr, tokens ? h->d_gv : nullptr, h->kpad, h->stream);
   stage_end(h, SCALE_STAGE_ATTENTION);
   return check_launch(e);
 }

@@ -195,64 +195,89 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
 // grid: cluster.
 //  1. soft-voting: each head's softmax maximum and normaliser over all candidates, combined from
 //     the chunk partials in chunk order; then per candidate the sum over heads, in head order.
+//     Token mode (kTok): the per-KV-head partial sums of the token scoring kernel are added in
+//     KV-head order instead.
 //  2. threshold: the sel_cnt-th largest score, by radix selection on the score bits, 8 bits a
 //     pass from the top (scores are >= 0, so their bit patterns order like their values); the
 //     digit is found with a prefix sum over the 256-bin histogram in descending digit order.
 //  3. selected = score above the threshold, or equal to it and among the first ties in index
-//     order; written in ascending block order by an ordered compaction.
-__global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(
-    const float* __restrict__ logits, const float2* __restrict__ head_stats, const ClusterGeo* __restrict__ geo,
-    int n_chunks, int cand_stride, int sink_blk, int num_q_heads, int top_k, int n_blocks,
-    float* __restrict__ spill, int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_cnt,
-    float* __restrict__ scores_out) {
+//     order; written in ascending index order by an ordered compaction.
+struct VoteArgs {
+  const float* logits;         // block mode: [cluster][Hq][cand_stride]
+  const float2* head_stats;    // block mode: [cluster][Hq][n_chunks]
+  const float* partial;        // token mode: [cluster][Hkv][cand_stride]
+  const ClusterGeo* geo;
+  int n_chunks, num_q_heads, num_kv_heads, top_k;
+  int64_t cand_stride;
+  int first;                   // index of candidate 0 (sink_blk, or sink_blk * B for tokens)
+  int n_out;                   // row length of scores_out
+  float* spill;                // [cluster][cand_stride]
+  int32_t *sel_idx, *sel_cnt;
+  float* scores_out;
+};
+
+template <bool kTok>
+__global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   __shared__ float score_lds[kMaxLdsCand];
   __shared__ int red_i[kVoteWaves];
   __shared__ unsigned hist[256];
   __shared__ int pick[2];
   extern __shared__ float head_lds[];               // [Hq] maxima, then [Hq] 1 / normaliser
   const int j = blockIdx.x;
-  const ClusterGeo G = geo[j];
+  const ClusterGeo G = a.geo[j];
   const int n = G.n_cand;
   const int cnt = G.sel_cnt;
-  float* score = n <= kMaxLdsCand ? score_lds : spill + (int64_t)j * cand_stride;
-  const float* x = logits + (int64_t)j * num_q_heads * cand_stride;
+  const int top_k = a.top_k;
+  float* score = n <= kMaxLdsCand ? score_lds : a.spill + (int64_t)j * a.cand_stride;
 
   // 1.
-  const int used = (n + kCandChunk - 1) / kCandChunk;
-  for (int h = threadIdx.x; h < num_q_heads; h += kVoteThreads) {
-    const float2* st = head_stats + ((int64_t)j * num_q_heads + h) * n_chunks;
-    float m = -FLT_MAX;
-    for (int k = 0; k < used; ++k) m = fmaxf(m, st[k].x);
-    float s = 0.f;
-    for (int k = 0; k < used; ++k) s += st[k].y * expf(st[k].x - m);
-    head_lds[h] = m;
-    head_lds[num_q_heads + h] = 1.0f / s;
-  }
-  __syncthreads();
-  for (int c = threadIdx.x; c < n; c += kVoteThreads) {
-    float acc = 0.f;
-    int h = 0;
-    for (; h + 16 <= num_q_heads; h += 16) {
-      float xv[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) xv[u] = x[(int64_t)(h + u) * cand_stride + c];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) acc += expf(xv[u] - head_lds[h + u]) * head_lds[num_q_heads + h + u];
+  if constexpr (kTok) {
+    const float* part = a.partial + (int64_t)j * a.num_kv_heads * a.cand_stride;
+    for (int c = threadIdx.x; c < n; c += kVoteThreads) {
+      float acc = 0.f;
+      for (int g = 0; g < a.num_kv_heads; ++g) acc += part[(int64_t)g * a.cand_stride + c];
+      score[c] = acc;
     }
-    for (; h < num_q_heads; ++h)
-      acc += expf(x[(int64_t)h * cand_stride + c] - head_lds[h]) * head_lds[num_q_heads + h];
-    score[c] = acc;
+  } else {
+    const int num_q_heads = a.num_q_heads;
+    const int64_t cand_stride = a.cand_stride;
+    const float* x = a.logits + (int64_t)j * num_q_heads * cand_stride;
+    const int used = (n + kCandChunk - 1) / kCandChunk;
+    for (int h = threadIdx.x; h < num_q_heads; h += kVoteThreads) {
+      const float2* st = a.head_stats + ((int64_t)j * num_q_heads + h) * a.n_chunks;
+      float m = -FLT_MAX;
+      for (int k = 0; k < used; ++k) m = fmaxf(m, st[k].x);
+      float s = 0.f;
+      for (int k = 0; k < used; ++k) s += st[k].y * expf(st[k].x - m);
+      head_lds[h] = m;
+      head_lds[num_q_heads + h] = 1.0f / s;
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < n; c += kVoteThreads) {
+      float acc = 0.f;
+      int h = 0;
+      for (; h + 16 <= num_q_heads; h += 16) {
+        float xv[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) xv[u] = x[(int64_t)(h + u) * cand_stride + c];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc += expf(xv[u] - head_lds[h + u]) * head_lds[num_q_heads + h + u];
+      }
+      for (; h < num_q_heads; ++h)
+        acc += expf(x[(int64_t)h * cand_stride + c] - head_lds[h]) * head_lds[num_q_heads + h];
+      score[c] = acc;
+    }
   }
   __syncthreads();
-  if (scores_out) {
-    float* so = scores_out + (int64_t)j * n_blocks;
-    for (int b = threadIdx.x; b < n_blocks; b += kVoteThreads) {
-      const int c = b - sink_blk;
+  if (a.scores_out) {
+    float* so = a.scores_out + (int64_t)j * a.n_out;
+    for (int b = threadIdx.x; b < a.n_out; b += kVoteThreads) {
+      const int c = b - a.first;
       so[b] = (c >= 0 && c < n) ? score[c] : -1.0f;
     }
   }
-  int32_t* out = sel_idx + (int64_t)j * top_k;
-  if (threadIdx.x == 0) sel_cnt[j] = cnt;
+  int32_t* out = a.sel_idx + (int64_t)j * top_k;
+  if (threadIdx.x == 0) a.sel_cnt[j] = cnt;
 
   // 2.
   unsigned prefix = 0, prefix_mask = 0;
@@ -313,7 +338,7 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(
         const unsigned u = __float_as_uint(score[c]);
         take = u > thr || (u == thr && ties_seen++ < want);
       }
-      if (take) out[pos++] = sink_blk + c;
+      if (take) out[pos++] = a.first + c;
     }
   }
   for (int i = cnt + threadIdx.x; i < top_k; i += kVoteThreads) out[i] = -1;
@@ -358,10 +383,42 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
                             float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                             hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
+  VoteArgs a{};
+  a.logits = logits;
+  a.head_stats = head_stats;
+  a.geo = geo;
+  a.n_chunks = selection_chunks(max_cand);
+  a.num_q_heads = num_q_heads;
+  a.top_k = top_k;
+  a.cand_stride = cand_stride;
+  a.first = sink_blk;
+  a.n_out = n_blocks;
+  a.spill = spill;
+  a.sel_idx = sel_idx;
+  a.sel_cnt = sel_cnt;
+  a.scores_out = scores_out;
   const size_t lds = sizeof(float) * 2 * (size_t)num_q_heads;
-  vote_topk_kernel<<<n_clusters, kVoteThreads, lds, stream>>>(logits, head_stats, geo, selection_chunks(max_cand),
-                                                          cand_stride, sink_blk, num_q_heads, top_k, n_blocks, spill,
-                                                          sel_idx, sel_cnt, scores_out);
+  vote_topk_kernel<false><<<n_clusters, kVoteThreads, lds, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
+                                   int first_token, int num_kv_heads, int top_k, int n_tokens, float* spill,
+                                   int32_t* sel_idx, int32_t* sel_cnt, float* scores_out, hipStream_t stream) {
+  if (n_clusters <= 0) return hipSuccess;
+  VoteArgs a{};
+  a.partial = partial;
+  a.geo = geo;
+  a.num_kv_heads = num_kv_heads;
+  a.top_k = top_k;
+  a.cand_stride = cand_stride;
+  a.first = first_token;
+  a.n_out = n_tokens;
+  a.spill = spill;
+  a.sel_idx = sel_idx;
+  a.sel_cnt = sel_cnt;
+  a.scores_out = scores_out;
+  vote_topk_kernel<true><<<n_clusters, kVoteThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -162,14 +162,14 @@ __device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u
   }
 }
 
-template <int D, int G, int RB, int LOG2B>
+template <int D, int G, int RB, int LOG2B, bool TOK>
 __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pages,
     const uint16_t* __restrict__ v_pages, const int32_t* __restrict__ block_table,
     const ClusterGeo* __restrict__ geo, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt, int top_k,
     int num_q_heads, int num_kv_heads, int n_blocks, float qk_scale_log2, int out_bf16,
-    void* __restrict__ out) {
+    void* __restrict__ out, const uint16_t* __restrict__ gk, const uint16_t* __restrict__ gv, int kpad) {
   using S = AttnShape<D, G, RB>;
   constexpr int B = 1 << LOG2B;
   constexpr int kTilesPerBlock = B / kKeyTile;
@@ -195,7 +195,9 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   int n_sel = sel_cnt[it.cluster];
   n_sel = n_sel < 0 ? 0 : (n_sel > top_k ? top_k : n_sel);
   const int n_sink_tiles = cg.sink_eff * kTilesPerBlock;
-  const int n_fixed = n_sink_tiles + n_sel * kTilesPerBlock;
+  // token-level selection: the selected keys are n_sel gathered rows, the last tile padded
+  const int n_fixed = n_sink_tiles + (TOK ? (n_sel + kKeyTile - 1) / kKeyTile : n_sel * kTilesPerBlock);
+  const int sel_rem = TOK ? n_sel % kKeyTile : 0;
   const int local0 = cg.lo_blk << LOG2B;
   const int local_end = p0 + it.n_rows;            // keys [local0, local_end) of the window
   const int n_tiles = n_fixed + (local_end - local0 + kKeyTile - 1) / kKeyTile;
@@ -209,6 +211,10 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
       int key0;
       if (t < n_sink_tiles) {
         key0 = t * kKeyTile;
+      } else if (TOK && t < n_fixed) {
+        // gathered row of the selection, marked by a negative entry
+        tile_row[batch & 1][i] = -1 - ((it.cluster * num_kv_heads + g) * kpad + (t - n_sink_tiles) * kKeyTile);
+        continue;
       } else if (t < n_fixed) {
         const int u = t - n_sink_tiles;
         int blk = sel[u / kTilesPerBlock];
@@ -225,7 +231,20 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
   // ---- per-thread prefetch registers: two sets, each one K and one V tile ----
   u32x4 kreg0[S::kPer], vreg0[2 * S::kVPer], kreg1[S::kPer], vreg1[2 * S::kVPer];
-  auto tile_base = [&](int t) -> int64_t { return (int64_t)tile_row[(t / kDescBatch) & 1][t % kDescBatch] * D; };
+  auto load_at = [&](int t, u32x4 (&kr)[S::kPer], u32x4 (&vr)[2 * S::kVPer]) {
+    const int r = tile_row[(t / kDescBatch) & 1][t % kDescBatch];
+    const uint16_t* kp = k_pages;
+    const uint16_t* vp = v_pages;
+    int64_t row = r;
+    if constexpr (TOK) {
+      if (r < 0) {
+        kp = gk;
+        vp = gv;
+        row = -1 - (int64_t)r;
+      }
+    }
+    load_tile<S, D>(kr, vr, kp, vp, row * D, tid);
+  };
 
   // ---- Q fragments: B operand of S^T = K Q^T for each 16-wide slice of d ----
   bf16x8 qf[D / 16];
@@ -261,9 +280,9 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   // and stored into LDS buffer j % 2 at the end of iteration j - 1. Loads past the last tile
   // re-read the last tile (never stored), which keeps the wait counts static.
   if (n_tiles > 0) {
-    load_tile<S, D>(kreg0, vreg0, k_pages, v_pages, tile_base(0), tid);
+    load_at(0, kreg0, vreg0);
     store_tile<S, D>(kreg0, vreg0, lds, tid);
-    load_tile<S, D>(kreg1, vreg1, k_pages, v_pages, tile_base(min(1, n_tiles - 1)), tid);
+    load_at(min(1, n_tiles - 1), kreg1, vreg1);
   }
   __syncthreads();
 
@@ -271,7 +290,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
                   u32x4 (&vs)[2 * S::kVPer]) {
     const int buf = t & 1;
     if (t > 0 && t % kDescBatch == 0 && t + kDescBatch < n_tiles) fill_batch(t / kDescBatch + 1);
-    load_tile<S, D>(kl, vl, k_pages, v_pages, tile_base(min(t + 2, n_tiles - 1)), tid);
+    load_at(min(t + 2, n_tiles - 1), kl, vl);
 
     const uint16_t* k_lds = lds + buf * S::kBufElems;
     const uint16_t* v_lds = k_lds + S::kKElems;
@@ -291,6 +310,17 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
       __builtin_amdgcn_sched_group_barrier(0x008, D / 16, 0);
     }
 
+    // Padding rows of a partial last gathered tile (keys sel_rem .. 63) take no weight.
+    if constexpr (TOK) {
+      if (sel_rem != 0 && t == n_fixed - 1) {
+        const int lim = sel_rem - 16 * half;     // accumulator e of block kb is key 32kb + 16half + e
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (32 * kb + e >= lim) s[kb][e] = -INFINITY;
+      }
+    }
     // Causal mask only on a local tile that reaches this wave's positions.
     if (t >= n_fixed) {
       const int key0 = local0 + (t - n_fixed) * kKeyTile;
@@ -387,15 +417,22 @@ struct LaunchArgs {
   float qk_scale_log2;
   int out_bf16;
   void* out;
+  const uint16_t *gk, *gv;
+  int kpad;
   hipStream_t stream;
 };
 
 template <int D, int G, int LOG2B>
 hipError_t launch_dgb(const LaunchArgs& a) {
   constexpr int RB = row_blocks(G);
-  sparse_attention_kernel<D, G, RB, LOG2B><<<a.n_items, G * RB * 64, 0, a.stream>>>(
-      a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
-      a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out);
+  if (a.gk)
+    sparse_attention_kernel<D, G, RB, LOG2B, true><<<a.n_items, G * RB * 64, 0, a.stream>>>(
+        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
+        a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, a.gk, a.gv, a.kpad);
+  else
+    sparse_attention_kernel<D, G, RB, LOG2B, false><<<a.n_items, G * RB * 64, 0, a.stream>>>(
+        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
+        a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, nullptr, nullptr, 0);
   return hipGetLastError();
 }
 
@@ -429,10 +466,12 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
                                    const WorkItem* items, int n_items, const int32_t* sel_idx,
                                    const int32_t* sel_cnt, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
-                                   float qk_scale_log2, int out_bf16, void* out, hipStream_t stream) {
+                                   float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
+                                   const uint16_t* gv, int kpad, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
-  const LaunchArgs a{q, k_pages, v_pages, block_table, geo, items, n_items, sel_idx, sel_cnt, top_k,
-                     num_q_heads, num_kv_heads, n_blocks, qk_scale_log2, out_bf16, out, stream};
+  const LaunchArgs a{q,           k_pages,      v_pages,  block_table, geo,        items,      n_items,
+                     sel_idx,     sel_cnt,      top_k,    num_q_heads, num_kv_heads, n_blocks, qk_scale_log2,
+                     out_bf16,    out,          gk,       gv,          kpad,       stream};
   const int group = num_q_heads / num_kv_heads;
   return head_dim == 128 ? launch_d<128>(group, block_size, a) : launch_d<64>(group, block_size, a);
 }

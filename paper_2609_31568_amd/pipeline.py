@@ -1,4 +1,5 @@
-"""One layer of cluster-level sparse prefill through the C ABI: rep keys -> select -> attention.
+"""One layer of cluster-level sparse prefill through the C ABI: rep keys -> select -> attention
+(block-level selection), or token selection -> attention (token-level selection).
 
 torch allocates the device buffers; the work runs in libscale's kernels.
 """
@@ -10,12 +11,12 @@ from .binding import SCALE_OUT_BF16, Scale, make_config
 
 
 def config_for(*, num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens, local_window,
-               max_tokens, max_clusters, out_bf16=False, softmax_scale=0.0, score_scale=0.0):
+               max_tokens, max_clusters, out_bf16=False, softmax_scale=0.0, score_scale=0.0, select_tokens=False):
     return make_config(num_q_heads=num_q_heads, num_kv_heads=num_kv_heads, head_dim=head_dim,
                        block_size=block_size, sub_chunk=sub_chunk, top_k=top_k, sink_tokens=sink_tokens,
                        local_window=local_window, max_tokens=max_tokens, max_clusters=max_clusters,
                        softmax_scale=softmax_scale, score_scale=score_scale,
-                       out_dtype=SCALE_OUT_BF16 if out_bf16 else 0)
+                       out_dtype=SCALE_OUT_BF16 if out_bf16 else 0, select_tokens=select_tokens)
 
 
 class LayerBuffers:
@@ -30,7 +31,8 @@ class LayerBuffers:
         self.sel_cnt = torch.empty((n_clusters,), dtype=torch.int32, device=device)
         odt = torch.bfloat16 if cfg.out_dtype == SCALE_OUT_BF16 else torch.float32
         self.out = torch.empty((n_tokens, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=device)
-        self.scores = torch.empty((n_clusters, nb), dtype=torch.float32, device=device) if with_scores else None
+        n_score = n_tokens if cfg.select_tokens else nb
+        self.scores = torch.empty((n_clusters, n_score), dtype=torch.float32, device=device) if with_scores else None
         self.fingerprints = (torch.empty((n_clusters, cfg.num_q_heads, cfg.head_dim), dtype=torch.float32,
                                          device=device) if with_scores else None)
 
@@ -38,7 +40,11 @@ class LayerBuffers:
 def run_layer(h: Scale, q, k_pages, v_pages, block_table, n_tokens: int, cluster_start, bufs: LayerBuffers):
     """Enqueue the whole hot path of one layer on the handle's stream (no synchronisation)."""
     cs = np.asarray(cluster_start, dtype=np.int32)
-    h.rep_keys(k_pages, block_table, n_tokens, bufs.k_rep)
-    h.select_cluster(q, n_tokens, bufs.k_rep, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores, bufs.fingerprints)
+    if h.cfg.select_tokens:
+        h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores,
+                                bufs.fingerprints)
+    else:
+        h.rep_keys(k_pages, block_table, n_tokens, bufs.k_rep)
+        h.select_cluster(q, n_tokens, bufs.k_rep, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores, bufs.fingerprints)
     h.sparse_prefill(q, k_pages, v_pages, block_table, n_tokens, cs, bufs.sel_idx, bufs.sel_cnt, bufs.out)
     return bufs

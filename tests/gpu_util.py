@@ -128,6 +128,98 @@ def check_scores(gpu_scores: np.ndarray, ref, num_kv_heads: int, what: str):
     return worst
 
 
+def token_candidates(d: dict, geo, block_size: int):
+    """Keys of every candidate token of each cluster (token-level selection), fp64 [n, Hkv, d]."""
+    n_max = max((g.sink_blk * block_size + g.n_cand for g in geo), default=0)
+    K = oracle.logical_rows(d["k_pages"], d["block_table"], np.arange(n_max), block_size)
+    return [K[g.sink_blk * block_size:g.sink_blk * block_size + g.n_cand] for g in geo]
+
+
+def token_score_bounds(ref, cands, num_kv_heads: int, score_scale: float = 1.0):
+    """First-order error bound of the GPU's token-level soft-voting scores, per candidate.
+
+    Logits: the fp32 fingerprint (one rounding) is split into two bf16 pieces (representation
+    error <= 2^-18 |v|) and multiplied with the exact bf16 keys in fp32 accumulation over 2 d
+    products: |dx| <= (2^-17 + (2 d + 8) u) sum_i |v_i k_i| =: dX. A softmax weight moves by at
+    most 2 p dX; the base-2 argument x log2(e) - lse carries u |x - lse| (R = logit range plus
+    log n); the normaliser is a sum of positive terms kept per lane over at most 2 n_tiles terms
+    with online rescaling (each step <= 4 u), merged over 5 lane levels and the chunks; the head sums
+    add Hq u. Hence |d score| <= score (2 dX + 3 u R + (4 (2 n_tiles + 6) + Hq + 16) u), plus an
+    absolute 1e-30 for weights that underflow.
+    """
+    out = []
+    for g, v, sc, K in zip(ref["geometry"], ref["fingerprints"], ref["scores"], cands):
+        if g.n_cand == 0:
+            out.append(np.zeros(0))
+            continue
+        Hq, d = v.shape
+        G = Hq // num_kv_heads
+        amax, xmin, xmax = 0.0, np.inf, -np.inf
+        rng = 0.0
+        for kv in range(num_kv_heads):
+            vg = v[kv * G:(kv + 1) * G]
+            Kg = K[:, kv, :]
+            amax = max(amax, float((np.abs(vg) @ np.abs(Kg).T).max()) * abs(score_scale))
+            x = (vg @ Kg.T) * score_scale
+            rng = max(rng, float((x.max(axis=1) - x.min(axis=1)).max()))
+        dX = (2.0 ** -17 + (2 * d + 8) * U32) * amax
+        R = rng + math.log(g.n_cand) + 1.0
+        n_tiles = -(-g.n_cand // 64)
+        rel = 2 * dX + 3 * U32 * R + (4 * (2 * n_tiles + 6) + Hq + 16) * U32
+        out.append(sc * rel + 1e-30)
+    return out
+
+
+def check_token_scores(gpu_scores: np.ndarray, ref, bounds, block_size: int, what: str):
+    """Candidate entries within the bound; every other entry of the row is -1."""
+    worst = 0.0
+    for j, (g, sc, bd) in enumerate(zip(ref["geometry"], ref["scores"], bounds)):
+        row = gpu_scores[j]
+        first = g.sink_blk * block_size
+        assert np.all(row[:first] == -1.0) and np.all(row[first + g.n_cand:] == -1.0), \
+            f"{what} cluster {j}: non-candidate entry is not -1"
+        if g.n_cand:
+            err = np.abs(row[first:first + g.n_cand].astype(np.float64) - sc)
+            assert np.all(err <= bd), f"{what} cluster {j}: score error {err.max():.2e} above bound"
+            worst = max(worst, float((err / np.maximum(sc, 1e-300)).max()))
+    return worst
+
+
+def check_token_selection(gpu_sel, gpu_cnt, gpu_scores, ref, bounds, block_size: int, what: str):
+    """The GPU selection is exactly the top-k of its own fp32 scores (score descending, position
+    ascending); against the oracle scores it is valid to twice the bound, and equal to the oracle's
+    wherever the oracle's gap at the threshold exceeds four times the bound."""
+    n_exact = 0
+    for j, (g, s_ref, sc, bd) in enumerate(zip(ref["geometry"], ref["selections"], ref["scores"], bounds)):
+        cnt = int(gpu_cnt[j])
+        assert cnt == g.sel_cnt, f"{what} cluster {j}: sel_cnt {cnt} != {g.sel_cnt}"
+        got = gpu_sel[j, :cnt].astype(np.int64)
+        assert np.all(gpu_sel[j, cnt:] == -1), f"{what} cluster {j}: padding is not -1"
+        assert np.all(np.diff(got) > 0), f"{what} cluster {j}: not strictly ascending"
+        first = g.sink_blk * block_size
+        if g.n_cand == 0:
+            continue
+        own = gpu_scores[j, first:first + g.n_cand].astype(np.float64)
+        order = np.lexsort((np.arange(g.n_cand), -own))
+        assert np.array_equal(np.sort(order[:cnt]) + first, got), f"{what} cluster {j}: not the top-k of its scores"
+        if cnt == g.n_cand:
+            assert np.array_equal(got, s_ref)
+            continue
+        if cnt == 0:
+            continue
+        eps = 2 * float(bd.max())
+        srt = np.sort(sc)[::-1]
+        kth = srt[cnt - 1]
+        chosen = np.zeros(g.n_cand, dtype=bool)
+        chosen[got - first] = True
+        assert np.all(sc[chosen] >= kth - eps), f"{what} cluster {j}: a selected token is not within eps of top-k"
+        assert np.all(sc[~chosen] <= kth + eps), f"{what} cluster {j}: an unselected token beats the k-th by > eps"
+        if srt[cnt - 1] - srt[cnt] > 2 * eps:
+            assert np.array_equal(got, s_ref), f"{what} cluster {j}: differs from the oracle above the margin"
+            n_exact += 1
+    return n_exact
+
+
 def check_selection(gpu_sel, gpu_cnt, ref, eps: float):
     """Exact where the oracle's margin exceeds MARGIN; eps-valid top-k everywhere."""
     n_exact = 0

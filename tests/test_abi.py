@@ -67,10 +67,16 @@ def _cfg(**over):
     (dict(block_size=32), -2),
     (dict(sub_chunk=192), -2),             # not a multiple of the block size
     (dict(num_q_heads=72, num_kv_heads=8), -2),   # group of 9 query heads
+    (dict(select_tokens=2), -1),
+    (dict(select_tokens=1, top_k=1 << 20, max_clusters=4096), -2),   # gathered rows past int32
 ])
 def test_init_rejects_bad_config_before_any_hip_call(over, status):
     pk = _pk()
+    over = dict(over)
+    raw_tokens = over.pop("select_tokens", None)
     cfg = _cfg(**over)
+    if raw_tokens is not None:
+        cfg.select_tokens = raw_tokens      # the raw field, past make_config's bool conversion
     h = ctypes.c_void_p(1234)
     st = pk.lib.scale_init(ctypes.byref(cfg), None, ctypes.byref(h))
     assert st == status
@@ -92,6 +98,7 @@ def test_calls_reject_null_handle():
     k = ctypes.c_int32()
     assert lib.scale_cluster_subchunks(None, 1, 128, 0, 0.95, 4096, 0, out.ctypes.data, ctypes.byref(k), None) == -1
     assert lib.scale_rep_keys_range(None, 1, None, 0, 128, 1) == -1
+    assert lib.scale_select_cluster_tokens(None, 1, 128, 1, None, cs.ctypes.data, 1, 1, 1, None, None) == -1
     lib.scale_free(None)        # no-op
 
 
@@ -121,6 +128,14 @@ def test_host_geometry_matches_oracle(name, c):
     assert geo.shape == (len(ref), 6)
     for row, g in zip(geo, ref):
         assert tuple(int(x) for x in row) == (g.s, g.e, g.lo_blk, g.sink_eff, g.n_cand, g.sel_cnt)
+    # token-level selection: candidates and the budget count tokens
+    k_tok = w.top_k * w.block_size + 37
+    cfg.select_tokens, cfg.top_k = 1, k_tok
+    geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
+    ref = oracle.geometry(w.n_tokens, w.sub_chunk, w.block_size, w.sink_tokens, w.local_window, k_tok, cs,
+                          select_tokens=True)
+    for row, g in zip(geo, ref):
+        assert g.tokens and tuple(int(x) for x in row) == (g.s, g.e, g.lo_blk, g.sink_eff, g.n_cand, g.sel_cnt)
 
 
 def test_geometry_short_last_subchunk_and_odd_clusters():

@@ -1,0 +1,213 @@
+"""GPU parity of token-level selection (paper Sec. 5.1.3, Eq. 9 over single tokens; Eq. 10 over
+the selected tokens): the HIP path through the C ABI against the fp64 oracle on the same seeded
+inputs -- scores within their error bound, the exact top-k of the GPU's own scores, oracle-equal
+selections above the margin, and the attention output under the GPU's selection."""
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_31568_amd  # noqa: F401  (fails loudly if the library is missing)
+
+    return torch.device("cuda:0")
+
+
+def _oracle(w, d, cs, k, with_output=True, external_sel=None):
+    return oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, sub_chunk=w.sub_chunk,
+                          block_size=w.block_size, top_k=k, sink_tokens=w.sink_tokens, local_window=w.local_window,
+                          cluster_start=cs, with_output=with_output, external_sel=external_sel, select_tokens=True)
+
+
+def _run(w, d, cs, dev, k, **over):
+    return gu.run_gpu(w, d, cs, dev, top_k=k, select_tokens=True, **over)
+
+
+SHAPES = {
+    # name: (workload, cluster size, token budget); budgets off the 64-row tile exercise the
+    # padding mask of the last gathered tile
+    "tiny_c4": (gen.WORKLOADS["tiny"], 4, 300),
+    "tiny_c1": (gen.WORKLOADS["tiny"], 1, 64),
+    "gqa128": (gen.Workload("gqa128", 1, 8, 2, 128, 8192, 128, 512, 3, 5, 128, 1024, 12, 1, 4, 31), 3, 603),
+    "g7": (gen.Workload("g7", 1, 14, 2, 128, 4096, 64, 256, 4, 6, 64, 512, 8, 1, 3, 32), 4, 333),
+    "g1": (gen.Workload("g1", 1, 2, 2, 64, 4096, 128, 512, 2, 3, 0, 700, 6, 1, 3, 33), 2, 200),
+    "g8": (gen.Workload("g8", 1, 8, 1, 64, 2048, 64, 128, 5, 4, 130, 100, 6, 1, 5, 34), 5, 130),
+}
+
+
+def _check_all(name, w, d, cs, k, res, ref):
+    B = w.block_size
+    cands = gu.token_candidates(d, ref["geometry"], B)
+    bounds = gu.token_score_bounds(ref, cands, w.num_kv_heads)
+    gu.check_rounding(res["fingerprints"], np.stack(ref["fingerprints"]), "fingerprints")
+    worst = gu.check_token_scores(res["scores"], ref, bounds, B, name)
+    # sel_idx rows hold k entries (the buffer keeps one column when k = 0)
+    n_exact = gu.check_token_selection(res["sel_idx"][:, :k], res["sel_cnt"], res["scores"], ref, bounds, B, name)
+    assert res["calls"] == len(cs) - 1
+    sels = gu.gpu_selections(res, len(cs) - 1)
+    own = _oracle(w, d, cs, k, external_sel=sels)
+    mx, rel = gu.check_output(res["out"], own["output"], f"{name} output")
+    gu.log(f"[tokens] {name}: worst relative score error {worst:.2e}; {n_exact} of {len(cs) - 1} clusters above "
+           f"the margin; output max-abs {mx:.2e} rel-L2 {rel:.2e}")
+    for j, g in enumerate(ref["geometry"]):
+        if np.array_equal(sels[j], ref["selections"][j]):
+            gu.check_output(res["out"][g.s:g.e], ref["output"][g.s:g.e], f"{name} cluster {j}")
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_token_small_shapes_full_parity(dev, name):
+    w, c, k = SHAPES[name]
+    gu.log(f"[tokens] {name} k={k}")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    res = _run(w, d, cs, dev, k)
+    ref = _oracle(w, d, cs, k)
+    _check_all(name, w, d, cs, k, res, ref)
+
+
+@pytest.mark.parametrize("k", [0, 1, 63, 65, 10 ** 6])
+def test_token_budget_edges(dev, k):
+    """Empty selection (sinks and window only), a single token (63 padding rows masked), budgets
+    one below and one above a tile, and the dense limit (every candidate selected)."""
+    w, c, _ = SHAPES["gqa128"]
+    gu.log(f"[tokens] budget {k}")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    res = _run(w, d, cs, dev, k)
+    ref = _oracle(w, d, cs, k)
+    if k >= 10 ** 6:
+        assert all(g.sel_cnt == g.n_cand for g in ref["geometry"])
+    _check_all(f"budget {k}", w, d, cs, k, res, ref)
+
+
+def test_token_mode_on_block_constant_keys_selects_whole_blocks(dev):
+    """Keys constant inside each block: every token of a block has the same score (bit for bit on
+    the GPU), so a budget of kb * B tokens takes whole blocks -- the blocks block-level selection
+    takes wherever its margin is clear -- and the two paths give the same attention."""
+    w, c, _ = SHAPES["gqa128"]
+    kb = 3
+    gu.log("[tokens] block-constant keys")
+    d = gen.make_layer(w)
+    d["k_pages"] = np.ascontiguousarray(np.broadcast_to(d["k_pages"][:, :, :1, :], d["k_pages"].shape))
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    tok = _run(w, d, cs, dev, kb * w.block_size)
+    blk = gu.run_gpu(w.with_(top_k=kb), d, cs, dev)
+    ref_blk = oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, sub_chunk=w.sub_chunk,
+                             block_size=w.block_size, top_k=kb, sink_tokens=w.sink_tokens,
+                             local_window=w.local_window, cluster_start=cs, with_output=False)
+    n_same = 0
+    for j, g in enumerate(ref_blk["geometry"]):
+        st = tok["sel_idx"][j, :tok["sel_cnt"][j]].astype(np.int64)
+        first = g.sink_blk * w.block_size
+        row = tok["scores"][j, first:first + g.n_cand * w.block_size].reshape(-1, w.block_size)
+        assert np.all(row == row[:, :1]), f"cluster {j}: token scores differ inside a block"
+        assert len(st) % w.block_size == 0 and np.all(np.diff(st.reshape(-1, w.block_size), axis=1) == 1)
+        if ref_blk["margins"][j] > gu.MARGIN:
+            sb = blk["sel_idx"][j, :blk["sel_cnt"][j]].astype(np.int64)
+            assert np.array_equal(st, oracle.selected_positions(g, sb, w.block_size))   # g: block geometry
+            gu.check_output(tok["out"][g.s:g.e], blk["out"][g.s:g.e], f"cluster {j} token vs block")
+            n_same += 1
+    assert n_same >= 1
+    gu.log(f"[tokens] block-constant keys: {n_same} of {len(cs) - 1} clusters compared")
+
+
+def test_token_deterministic_and_page_permutation(dev):
+    w, c, k = SHAPES["g7"]
+    gu.log("[tokens] determinism + paging")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    a = _run(w, d, cs, dev, k)
+    b = _run(w, d, cs, dev, k)
+    for key in ("sel_idx", "sel_cnt", "out", "scores", "fingerprints"):
+        assert np.array_equal(a[key], b[key]), key
+    perm = np.random.default_rng(4).permutation(w.n_blocks)
+    kp = np.empty_like(d["k_pages"])
+    vp = np.empty_like(d["v_pages"])
+    kp[perm] = d["k_pages"]
+    vp[perm] = d["v_pages"]
+    p = _run(w, dict(d, k_pages=kp, v_pages=vp, block_table=perm.astype(np.int32)), cs, dev, k)
+    for key in ("sel_idx", "sel_cnt", "out", "scores"):
+        assert np.array_equal(a[key], p[key]), key
+
+
+def test_token_exact_ties_pick_lowest_position(dev):
+    """Copies of the best token's key (all KV heads) score identically; the lowest positions win."""
+    w, _, _ = SHAPES["gqa128"]
+    k = 2
+    gu.log("[tokens] exact ties")
+    d = gen.make_layer(w)
+    cs = np.array([0, 12, 16], dtype=np.int32)
+    ref0 = _oracle(w, d, cs, k, with_output=False)
+    g = ref0["geometry"][1]
+    B = w.block_size
+    first = g.sink_blk * B
+    best = first + int(np.argmax(ref0["scores"][1]))
+    rng = np.random.default_rng(5)
+    dups = sorted(int(t) for t in rng.choice([t for t in range(first, first + g.n_cand) if t != best], 3,
+                                             replace=False))
+    src = d["k_pages"][d["block_table"][best // B], :, best % B, :].copy()
+    for t in dups:
+        d["k_pages"][d["block_table"][t // B], :, t % B, :] = src
+    res = _run(w, d, cs, dev, k)
+    ref = _oracle(w, d, cs, k, with_output=False)
+    tied = sorted(dups + [best])
+    assert list(ref["selections"][1]) == tied[:2]
+    assert list(res["sel_idx"][1, :2]) == tied[:2]
+
+
+@pytest.mark.parametrize("name,c,n_sample,seed", [("llama128k", 8, 6, 11), ("llama32k", 1, 8, 12)])
+def test_token_full_size_sampled(dev, name, c, n_sample, seed):
+    """Llama-3-8B-shaped layers at full context with a budget of 32 blocks' worth of tokens: the
+    GPU runs the whole layer; sampled clusters are checked against the oracle (scores, selection)
+    with their first and last 32-row attention tiles under the GPU's selection."""
+    w = gen.WORKLOADS[name].with_(cluster=c)
+    k = 32 * w.block_size
+    gu.log(f"[tokens] {name} c={c}: generating")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    J = len(cs) - 1
+    rng = np.random.default_rng(seed)
+    clusters = sorted({J - 1, *rng.choice(np.arange(1, J - 1), size=n_sample - 1, replace=False).tolist()})
+    geo = oracle.geometry(w.n_tokens, w.sub_chunk, w.block_size, w.sink_tokens, w.local_window, k, cs,
+                          select_tokens=True)
+    rows = gu.sample_rows([geo[j] for j in clusters], rng, tiles_per_cluster=0)
+    gu.log(f"[tokens] {name}: GPU, {J} clusters")
+    res = _run(w, d, cs, dev, k, out_rows=np.concatenate(rows))
+    assert res["calls"] == J
+    gu.log(f"[tokens] {name}: oracle on clusters {clusters}")
+    B = w.block_size
+    ref = {"geometry": [], "fingerprints": [], "scores": [], "selections": []}
+    for j in clusters:
+        g = geo[j]
+        v = oracle.anchor_fingerprint(d["q"], g.s, g.anchor_end)
+        K = oracle.logical_rows(d["k_pages"], d["block_table"], np.arange(g.sink_blk * B, g.sink_blk * B + g.n_cand), B)
+        sc = oracle.soft_vote(oracle.block_logits(v, K, w.num_kv_heads))
+        sel, _ = oracle.select_topk(sc, g.sink_blk * B, k)
+        for key, val in (("geometry", g), ("fingerprints", v), ("scores", sc), ("selections", sel)):
+            ref[key].append(val)
+    cands = gu.token_candidates(d, ref["geometry"], B)
+    bounds = gu.token_score_bounds(ref, cands, w.num_kv_heads)
+    gu.check_rounding(res["fingerprints"][clusters], np.stack(ref["fingerprints"]), "fingerprints")
+    worst = gu.check_token_scores(res["scores"][clusters], ref, bounds, B, name)
+    n_exact = gu.check_token_selection(res["sel_idx"][clusters], res["sel_cnt"][clusters], res["scores"][clusters],
+                                       ref, bounds, B, name)
+    gu.log(f"[tokens] {name}: worst relative score error {worst:.2e}; {n_exact} of {len(clusters)} sampled "
+           f"clusters above the margin")
+    sels = gu.gpu_selections(res, J)
+    at = 0
+    for i, j in enumerate(clusters):
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], geo[j], sels[j], rows[i],
+                                      B)
+        mx, rel = gu.check_output(res["out"][at:at + len(rows[i])], o_ref, f"{name} cluster {j}")
+        at += len(rows[i])
+    gu.log(f"[tokens] {name}: sampled attention ok")
