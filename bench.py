@@ -11,6 +11,10 @@ local window.
 Prints ONE JSON line (rank 0) with the throughput, the roofline of the dominant kernel
 (attention, bf16 MFMA), HBM rates of the selection kernels, retrieval-call counts and the fp64
 oracle timed on a bounded sample on the host's cores.
+
+Other modes (one JSON line each, no CPU baseline unless stated): --sweep over cluster sizes,
+--theta / --theta-sweep with clusters formed on the GPU by anchor-based clustering, and
+--tokens K for token-level selection with a budget of K tokens.
 """
 from __future__ import annotations
 
@@ -45,6 +49,8 @@ def parse_args():
     ap.add_argument("--outer", type=int, default=0, help="outer chunk in sub-chunks for --theta (0: whole context)")
     ap.add_argument("--overlap", action="store_true",
                     help="also report the top-k overlap ratio (Eq. 7) of the clusters against per-sub-chunk selection")
+    ap.add_argument("--tokens", type=int, default=0,
+                    help="token-level selection with this budget in tokens (0: block-level selection)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
     ap.add_argument("--out-bf16", action="store_true")
@@ -75,23 +81,37 @@ def measured_traffic(workload_name):
     return int(block["traffic_bytes"])
 
 
-def geometry_work(w, geo):
+def geometry_work(w, geo, tokens=False):
     """Algorithmic attention FLOPs and the selection-side bytes from the cluster geometry.
 
     Attention: 4 d Hq per (query row, visible key) pair (two products of 2 d FLOP), over
-    exactly the keys of Eq. 10 -- masked pairs are not work.
+    exactly the keys of Eq. 10 -- masked pairs are not work. With token-level selection, n_cand
+    and sel_cnt count tokens.
     """
     B, d, Hq, Hkv = w.block_size, w.head_dim, w.num_q_heads, w.num_kv_heads
     pairs = 0
     for s, e, lo_blk, sink_eff, n_cand, sel_cnt in geo.tolist():
         rows = e - s
-        fixed = (sink_eff + sel_cnt) * B
+        fixed = sink_eff * B + sel_cnt * (1 if tokens else B)
         base = lo_blk * B
         pairs += rows * fixed + (sum(range(s - base + 1, e - base + 1)))
     n_clusters = len(geo)
     nb = w.n_tokens // B
     anchor_rows = sum(min(e, s + w.sub_chunk) - s for s, e, *_ in geo.tolist())
     n_cand = int(geo[:, 4].sum())
+    if tokens:
+        max_cand = int(geo[:, 4].max()) if len(geo) else 0
+        n_sel = int(geo[:, 5].sum())
+        return {
+            "attention_flops": 4.0 * d * Hq * pairs,
+            "pairs": pairs,
+            "fingerprint_bytes": anchor_rows * Hq * d * 2 + n_clusters * Hq * d * 4,
+            # every candidate key read once, and one logit (2 d FLOP) per (cluster, head, token)
+            "token_logits_bytes": max_cand * Hkv * d * 2,
+            "token_logits_flops": 2.0 * d * Hq * n_cand,
+            "vote_bytes": n_cand * Hkv * 4,
+            "gather_bytes": 2 * 2 * n_sel * Hkv * d * 2,
+        }
     return {
         "attention_flops": 4.0 * d * Hq * pairs,
         "pairs": pairs,
@@ -178,10 +198,11 @@ def time_path(args, w, c, layers, dev, theta=None):
 
     l_max = args.l_max or 8 * w.sub_chunk
     max_clusters = w.n_sub_chunks if theta is not None else len(gen.cluster_starts(w.n_sub_chunks, c)) - 1
+    tokens = args.tokens > 0
     cfg = pk.config_for(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
-                        block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=w.top_k, sink_tokens=w.sink_tokens,
-                        local_window=w.local_window, max_tokens=w.n_tokens, max_clusters=max_clusters,
-                        out_bf16=args.out_bf16)
+                        block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=args.tokens if tokens else w.top_k,
+                        sink_tokens=w.sink_tokens, local_window=w.local_window, max_tokens=w.n_tokens,
+                        max_clusters=max_clusters, out_bf16=args.out_bf16, select_tokens=tokens)
     h = pk.Scale(cfg)
     if theta is None:
         cs = gen.cluster_starts(w.n_sub_chunks, c)
@@ -190,7 +211,7 @@ def time_path(args, w, c, layers, dev, theta=None):
         layer_cs = [h.cluster_subchunks(q, w.n_tokens, theta, l_max, args.outer) for q, *_ in layers]
         cs = layer_cs[0]
     geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
-    work = geometry_work(w, geo)
+    work = geometry_work(w, geo, tokens)
     # one set of outputs shared by the layers: each layer's output is complete when its attention
     # call ends, and the next layer's calls are ordered after it on the stream
     bufs = pk.LayerBuffers(cfg, w.n_tokens, max_clusters, device=dev)
@@ -198,10 +219,12 @@ def time_path(args, w, c, layers, dev, theta=None):
     def step():
         for (q, kp, vp, bt), lcs in zip(layers, layer_cs):
             if theta is not None:
-                h.rep_keys(kp, bt, w.n_tokens, bufs.k_rep)
                 lcs = h.cluster_subchunks(q, w.n_tokens, theta, l_max, args.outer)
-                h.select_cluster(q, w.n_tokens, bufs.k_rep, lcs, bufs.sel_idx, bufs.sel_cnt, bufs.scores,
-                                 bufs.fingerprints)
+                if tokens:
+                    h.select_cluster_tokens(q, w.n_tokens, kp, bt, lcs, bufs.sel_idx, bufs.sel_cnt)
+                else:
+                    h.rep_keys(kp, bt, w.n_tokens, bufs.k_rep)
+                    h.select_cluster(q, w.n_tokens, bufs.k_rep, lcs, bufs.sel_idx, bufs.sel_cnt)
                 h.sparse_prefill(q, kp, vp, bt, w.n_tokens, lcs, bufs.sel_idx, bufs.sel_cnt, bufs.out)
             else:
                 pk.run_layer(h, q, kp, vp, bt, w.n_tokens, lcs, bufs)
@@ -220,7 +243,7 @@ def time_path(args, w, c, layers, dev, theta=None):
     t1 = time.perf_counter()
     stages = h.stage_times(reset=True)
     calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
-    overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap else None
+    overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap and not tokens else None
     h.close()
     del bufs
 
@@ -233,7 +256,23 @@ def time_path(args, w, c, layers, dev, theta=None):
     def gbs(nbytes, ms):
         return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
 
-    hbm = {
+    if tokens:
+        lg_ms = per_launch["logits"]
+        hbm = {
+            "fingerprint": {"GB/s": gbs(work["fingerprint_bytes"], per_launch["fingerprint"]),
+                            "bytes": work["fingerprint_bytes"]},
+            "token_logits": {"GB/s": gbs(work["token_logits_bytes"], lg_ms), "bytes": work["token_logits_bytes"],
+                             "TFLOP/s": round(work["token_logits_flops"] / (lg_ms * 1e-3) / 1e12, 2) if lg_ms else None,
+                             "flops": work["token_logits_flops"],
+                             "note": "split + stats pass + log-normaliser + scores pass; bytes = one read of every "
+                                     "candidate key, flops = one logit per (cluster, head, candidate token)"},
+            "vote_topk": {"GB/s": gbs(work["vote_bytes"], per_launch["vote_topk"]), "bytes": work["vote_bytes"]},
+            "gather": {"GB/s": gbs(work["gather_bytes"], per_launch["gather"]), "bytes": work["gather_bytes"]},
+            "peak_GB/s": PEAK_HBM_GBS,
+        }
+    else:
+        hbm = None
+    hbm = hbm or {
         "rep_keys": {"GB/s": gbs(work["rep_keys_bytes"], per_launch["rep_keys"]), "bytes": work["rep_keys_bytes"]},
         "fingerprint": {"GB/s": gbs(work["fingerprint_bytes"], per_launch["fingerprint"]),
                         "bytes": work["fingerprint_bytes"]},
@@ -262,7 +301,8 @@ def time_path(args, w, c, layers, dev, theta=None):
             "n_tokens": w.n_tokens, "layers": w.layers, "num_q_heads": w.num_q_heads,
             "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "block_size": w.block_size,
             "sub_chunk": w.sub_chunk, "cluster": c if theta is None else f"anchor clustering, theta {theta}",
-            "top_k": w.top_k, "sink_tokens": w.sink_tokens,
+            "top_k": w.top_k if not tokens else None,
+            "select_tokens": args.tokens if tokens else None, "sink_tokens": w.sink_tokens,
             "local_window": w.local_window, "out_dtype": "bf16" if args.out_bf16 else "fp32",
             "seed": w.seed,
         },
@@ -273,7 +313,8 @@ def time_path(args, w, c, layers, dev, theta=None):
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": measured_traffic(w.name) if theta is None and c == gen.WORKLOADS[w.name].cluster else None,
+            "traffic": (measured_traffic(w.name) if theta is None and not tokens and c == gen.WORKLOADS[w.name].cluster
+                        else None),
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
         },
@@ -384,7 +425,7 @@ def main():
         wc = w.with_(cluster=c)
         print(f"[bench] timing " + (f"theta={theta}" if theta is not None else f"c={c}"), file=sys.stderr, flush=True)
         result, cs, geo = time_path(args, wc, c, layers, dev, theta=theta)
-        if rank == 0 and not args.no_cpu_baseline:
+        if rank == 0 and not args.no_cpu_baseline and not args.tokens:
             print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
             result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles)
         if rank == 0:

@@ -88,11 +88,13 @@ hipError_t launch_token_selection(const float* fingerprints, const uint16_t* k_p
                                   float score_scale, int64_t cand_stride, uint16_t* F, float2* stats, float* lse2,
                                   float* partial, hipStream_t stream);
 
-// Score = sum of the partials over KV heads, then the deterministic top-k of vote_topk; entries are
-// token positions first_token + c. scores_out (optional) rows have n_tokens entries.
+// Score = sum of the partials over KV heads (into spill [cluster][cand_stride]), then the
+// deterministic top-k of vote_topk; entries are token positions first_token + c. scores_out
+// (optional) rows have n_tokens entries.
 hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
-                                   int first_token, int num_kv_heads, int top_k, int n_tokens, float* spill,
-                                   int32_t* sel_idx, int32_t* sel_cnt, float* scores_out, hipStream_t stream);
+                                   int max_cand, int first_token, int num_kv_heads, int top_k, int n_tokens,
+                                   float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                   hipStream_t stream);
 
 // Selected keys and values of every cluster copied to gk / gv [cluster][Hkv][kpad][d] in selection
 // order, kpad = top_k rounded up to kTokenTile; the rows of the last partial tile past sel_cnt are

@@ -433,9 +433,9 @@ scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int3
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
   stage_begin(h);
-  st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, c.max_tokens, first_token,
-                                                   c.num_kv_heads, c.top_k, n_tokens, h->d_tok_score, sel_idx,
-                                                   sel_cnt, scores_out, h->stream));
+  st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, c.max_tokens, max_cand,
+                                                   first_token, c.num_kv_heads, c.top_k, n_tokens, h->d_tok_score,
+                                                   sel_idx, sel_cnt, scores_out, h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
   h->retrieval_calls += n_clusters;

@@ -169,6 +169,7 @@ __global__ __launch_bounds__(kThreads) void block_logits_kernel(
 constexpr int kVoteThreads = 1024;
 constexpr int kVoteWaves = kVoteThreads / 64;
 constexpr int kMaxLdsCand = 8192;        // scores of larger clusters live in the global spill row
+constexpr int kHistBins = 4096;          // radix digits of the first two passes (12 bits)
 
 // Exclusive prefix sum over the work-group's threads in thread order; the total through *total.
 __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
@@ -197,9 +198,11 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
 //     the chunk partials in chunk order; then per candidate the sum over heads, in head order.
 //     Token mode (kTok): the per-KV-head partial sums of the token scoring kernel are added in
 //     KV-head order instead.
-//  2. threshold: the sel_cnt-th largest score, by radix selection on the score bits, 8 bits a
-//     pass from the top (scores are >= 0, so their bit patterns order like their values); the
-//     digit is found with a prefix sum over the 256-bin histogram in descending digit order.
+//  2. threshold: the sel_cnt-th largest score, by radix selection on the score bits (scores are
+//     >= 0, so their bit patterns order like their values and the sign bit is 0) in three passes
+//     over bits 30-19, 18-7 and 6-0; wide first digits spread the scores of a cluster, which share
+//     few exponents, over many histogram bins. The digit is found with a prefix sum over the
+//     histogram in descending digit order.
 //  3. selected = score above the threshold, or equal to it and among the first ties in index
 //     order; written in ascending index order by an ordered compaction.
 struct VoteArgs {
@@ -220,7 +223,7 @@ template <bool kTok>
 __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   __shared__ float score_lds[kMaxLdsCand];
   __shared__ int red_i[kVoteWaves];
-  __shared__ unsigned hist[256];
+  __shared__ unsigned hist[kHistBins];
   __shared__ int pick[2];
   extern __shared__ float head_lds[];               // [Hq] maxima, then [Hq] 1 / normaliser
   const int j = blockIdx.x;
@@ -232,12 +235,7 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
 
   // 1.
   if constexpr (kTok) {
-    const float* part = a.partial + (int64_t)j * a.num_kv_heads * a.cand_stride;
-    for (int c = threadIdx.x; c < n; c += kVoteThreads) {
-      float acc = 0.f;
-      for (int g = 0; g < a.num_kv_heads; ++g) acc += part[(int64_t)g * a.cand_stride + c];
-      score[c] = acc;
-    }
+    score = a.spill + (int64_t)j * a.cand_stride;   // written by token_sum_kernel
   } else {
     const int num_q_heads = a.num_q_heads;
     const int64_t cand_stride = a.cand_stride;
@@ -279,69 +277,146 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   int32_t* out = a.sel_idx + (int64_t)j * top_k;
   if (threadIdx.x == 0) a.sel_cnt[j] = cnt;
 
+  // f(score bits) for every candidate, in any order. Token mode reads the global score row as
+  // float4s (n is a multiple of 64, the row 16-byte aligned) with four loads in flight per thread.
+  auto sweep = [&](auto&& f) {
+    if constexpr (kTok) {
+      const float4* s4 = reinterpret_cast<const float4*>(score);
+      const int n4 = n >> 2;
+      for (int b = threadIdx.x; b < n4; b += 4 * kVoteThreads) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = s4[min(b + u * kVoteThreads, n4 - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (b + u * kVoteThreads < n4) {
+            f(__float_as_uint(v[u].x));
+            f(__float_as_uint(v[u].y));
+            f(__float_as_uint(v[u].z));
+            f(__float_as_uint(v[u].w));
+          }
+        }
+      }
+    } else {
+      for (int c = threadIdx.x; c < n; c += kVoteThreads) f(__float_as_uint(score[c]));
+    }
+  };
+  // f(index, score bits) for the candidates [c0, c1) in index order (token mode: c0, c1 multiples
+  // of 4, float4 loads, four in flight).
+  auto range_each = [&](int c0, int c1, auto&& f) {
+    if constexpr (kTok) {
+      const float4* s4 = reinterpret_cast<const float4*>(score);
+      for (int c = c0; c < c1; c += 16) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = s4[min(c + 4 * u, c1 - 4) >> 2];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (c + 4 * u < c1) {
+            f(c + 4 * u, __float_as_uint(v[u].x));
+            f(c + 4 * u + 1, __float_as_uint(v[u].y));
+            f(c + 4 * u + 2, __float_as_uint(v[u].z));
+            f(c + 4 * u + 3, __float_as_uint(v[u].w));
+          }
+        }
+      }
+    } else {
+      for (int c = c0; c < c1; ++c) f(c, __float_as_uint(score[c]));
+    }
+  };
+
   // 2.
   unsigned prefix = 0, prefix_mask = 0;
   int want = cnt;             // rank (1-based) of the threshold among the still-matching values
   if (cnt > 0 && cnt < n) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (threadIdx.x < 256) hist[threadIdx.x] = 0;
+    for (int pass = 0; pass < 3; ++pass) {
+      const int shift = pass == 0 ? 19 : (pass == 1 ? 7 : 0);
+      const int nbins = pass == 2 ? 128 : kHistBins;
+      const unsigned dmask = (unsigned)nbins - 1u;
+      for (int b = threadIdx.x; b < nbins; b += kVoteThreads) hist[b] = 0;
       __syncthreads();
-      for (int c = threadIdx.x; c < n; c += kVoteThreads) {
-        const unsigned u = __float_as_uint(score[c]);
-        if ((u & prefix_mask) == prefix) atomicAdd(&hist[(u >> shift) & 0xFF], 1u);
-      }
+      sweep([&](unsigned u) {
+        if ((u & prefix_mask) == prefix) atomicAdd(&hist[(u >> shift) & dmask], 1u);
+      });
       __syncthreads();
-      const int h_cnt = threadIdx.x < 256 ? (int)hist[255 - threadIdx.x] : 0;
+      // thread t owns the `per` digits below nbins - 1 - t * per, in descending order
+      const int per = (nbins + kVoteThreads - 1) / kVoteThreads;
+      const int top = nbins - 1 - (int)threadIdx.x * per;
+      int local = 0;
+      for (int i = 0; i < per; ++i)
+        if (top - i >= 0) local += (int)hist[top - i];
       int total = 0;
-      const int above = block_exclusive_scan(h_cnt, red_i, &total);   // values with a larger digit
-      if (threadIdx.x < 256 && above < want && above + h_cnt >= want) {
-        pick[0] = 255 - threadIdx.x;
-        pick[1] = above;
+      const int above = block_exclusive_scan(local, red_i, &total);   // values with a larger digit
+      if (above < want && above + local >= want) {
+        int acc = above;
+        for (int i = 0; i < per; ++i) {
+          const int hc = (int)hist[top - i];
+          if (acc + hc >= want) {
+            pick[0] = top - i;
+            pick[1] = acc;
+            break;
+          }
+          acc += hc;
+        }
       }
       __syncthreads();
       want -= pick[1];
       prefix |= (unsigned)pick[0] << shift;
-      prefix_mask |= 0xFFu << shift;
+      prefix_mask |= dmask << shift;
       __syncthreads();
     }
   }
   const unsigned thr = prefix;   // bit pattern of the threshold value (valid when 0 < cnt < n)
 
-  // 3. thread t owns a contiguous index range, so prefix sums follow index order.
-  const int per = (n + kVoteThreads - 1) / kVoteThreads;
-  const int c0 = min(n, threadIdx.x * per), c1 = min(n, c0 + per);
-  int n_tie = 0, n_sel_local = 0;
-  if (cnt >= n) {
-    n_sel_local = c1 - c0;
-  } else if (cnt > 0) {
-    for (int c = c0; c < c1; ++c) n_tie += (__float_as_uint(score[c]) == thr);
+  // 3. thread t owns a contiguous index range, so prefix sums follow index order. The ties at
+  //    the threshold taken are the first `want` in index order: this thread's ties are the
+  //    global ties [tie_before, tie_before + n_tie).
+  int per = (n + kVoteThreads - 1) / kVoteThreads;
+  if (kTok) per = (per + 3) & ~3;
+  const int c0 = min(n, (int)threadIdx.x * per), c1 = min(n, c0 + per);
+  int n_tie = 0, n_gt = 0;
+  if (cnt > 0 && cnt < n) {
+    range_each(c0, c1, [&](int, unsigned u) {
+      n_gt += u > thr;
+      n_tie += u == thr;
+    });
   }
   int tie_total = 0;
   const int tie_before = block_exclusive_scan(n_tie, red_i, &tie_total);
-  if (cnt > 0 && cnt < n) {
-    int ties_seen = tie_before;
-    for (int c = c0; c < c1; ++c) {
-      const unsigned u = __float_as_uint(score[c]);
-      if (u > thr) ++n_sel_local;
-      else if (u == thr && ties_seen++ < want) ++n_sel_local;
-    }
-  }
+  const int n_sel_local = cnt >= n ? c1 - c0 : (cnt > 0 ? n_gt + min(max(want - tie_before, 0), n_tie) : 0);
   int sel_total = 0;
   int pos = block_exclusive_scan(n_sel_local, red_i, &sel_total);
-  if (cnt > 0) {
+  if (cnt >= n) {
+    for (int c = c0; c < c1; ++c) out[pos++] = a.first + c;
+  } else if (cnt > 0) {
     int ties_seen = tie_before;
-    for (int c = c0; c < c1; ++c) {
-      bool take;
-      if (cnt >= n) {
-        take = true;
-      } else {
-        const unsigned u = __float_as_uint(score[c]);
-        take = u > thr || (u == thr && ties_seen++ < want);
-      }
+    range_each(c0, c1, [&](int c, unsigned u) {
+      const bool take = u > thr || (u == thr && ties_seen++ < want);
       if (take) out[pos++] = a.first + c;
-    }
+    });
   }
   for (int i = cnt + threadIdx.x; i < top_k; i += kVoteThreads) out[i] = -1;
+}
+
+// grid: (1024-candidate slice, cluster). score[j][c] = sum over KV heads g, in order, of the
+// partial scores of the token scoring kernel; four candidates per thread (n_cand is a multiple of
+// 64 and the rows are 16-byte aligned).
+__global__ __launch_bounds__(kThreads) void token_sum_kernel(const float* __restrict__ partial,
+                                                             const ClusterGeo* __restrict__ geo, int64_t cand_stride,
+                                                             int num_kv_heads, float* __restrict__ score) {
+  const int j = blockIdx.y;
+  const int c = (blockIdx.x * kThreads + threadIdx.x) * 4;
+  if (c >= geo[j].n_cand) return;
+  const float* part = partial + (int64_t)j * num_kv_heads * cand_stride + c;
+  float4 acc = *reinterpret_cast<const float4*>(part);
+  for (int g = 1; g < num_kv_heads; ++g) {
+    const float4 v = *reinterpret_cast<const float4*>(part + (int64_t)g * cand_stride);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  *reinterpret_cast<float4*>(score + (int64_t)j * cand_stride + c) = acc;
 }
 
 }  // namespace
@@ -403,9 +478,16 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
 }
 
 hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
-                                   int first_token, int num_kv_heads, int top_k, int n_tokens, float* spill,
-                                   int32_t* sel_idx, int32_t* sel_cnt, float* scores_out, hipStream_t stream) {
+                                   int max_cand, int first_token, int num_kv_heads, int top_k, int n_tokens,
+                                   float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                   hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
+  if (max_cand > 0) {
+    const dim3 grid((unsigned)((max_cand + 4 * kThreads - 1) / (4 * kThreads)), (unsigned)n_clusters);
+    token_sum_kernel<<<grid, kThreads, 0, stream>>>(partial, geo, cand_stride, num_kv_heads, spill);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   VoteArgs a{};
   a.partial = partial;
   a.geo = geo;

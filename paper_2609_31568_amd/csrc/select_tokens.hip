@@ -13,15 +13,15 @@
 //  split          fingerprints -> bf16 pieces F[g][row][piece][d], row = j * GP + i (GP = the
 //                 group size rounded up to a power of two; rows i >= G are zero)
 //  token_logits   (KV head g, row group of 128 rows, chunk of tiles):
-//                   stats pass   per (row, chunk): max and sum of 2^(x - max) over the chunk's
-//                                candidates (x = logit in base-2 units), merged online
+//                   stats pass   per (row, chunk): a reference m and s = sum of 2^(x - m) over the
+//                                chunk's candidates (x = logit in base-2 units)
 //                   scores pass  per (cluster, KV head, token): sum over the query heads of g of
 //                                2^(x - lse_row), written as a partial score
-//  token_lse      per row: log2 of the softmax normaliser, the chunk partials merged in chunk order
+//  token_lse      per row: log2 of the softmax normaliser from the chunk partials (fixed order)
 //  gather         (tile of selected rows, KV head, cluster) -> the selected keys and values copied
 //                 into [cluster][g][kpad][d] tiles; rows past the selection are zero
 //
-// The soft-voting sum over KV heads and the top-k run in vote_topk (select.hip). Every
+// The soft-voting sum over KV heads (token_sum) and the top-k (vote_topk) are in select.hip. Every
 // reduction has a fixed order, so two runs give identical bits.
 #include <math.h>
 
@@ -41,6 +41,7 @@ constexpr int kTokThreads = 256;      // 4 waves, one 32-row block each
 constexpr int kRowsPerGroup = 128;
 constexpr int kTargetGroups = 2048;
 constexpr int kGatherThreads = 256;
+constexpr float kStatsHeadroom = 20.f;   // base-2 units a logit may exceed the stats reference by
 
 __device__ __forceinline__ uint16_t bf16_rne(float v) {
   uint32_t u = __float_as_uint(v);
@@ -190,9 +191,9 @@ __global__ __launch_bounds__(kTokThreads) void token_logits_kernel(TokArgs a) {
         acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][c], k0, acc[0], 0, 0, 0);
         acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][c], k1, acc[1], 0, 0, 0);
       }
+      if constexpr (kScores) {
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        if constexpr (kScores) {
+        for (int cb = 0; cb < 2; ++cb) {
           float p[16];
 #pragma unroll
           for (int e = 0; e < 16; ++e)
@@ -210,18 +211,29 @@ __global__ __launch_bounds__(kTokThreads) void token_logits_kernel(TokArgs a) {
             if ((GP < 8 || half == 0) && tc < nc[e])
               a.partial[((int64_t)j * a.num_kv_heads + g) * a.cand_stride + tc + 32 * cb + col] = sum;
           }
-        } else {
+        }
+      } else {
+        // s accumulates 2^(x - m) against a reference m that is only raised (exactly: s rescaled)
+        // when a value would exceed it by more than 2^kStatsHeadroom; the first tile always does.
+        bool up = false;
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          up |= tc < nc[e] && fmaxf(acc[0][e] * a.scale2, acc[1][e] * a.scale2) > m[e] + kStatsHeadroom;
+        if (__any(up)) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const float x = acc[cb][e] * a.scale2;
-            const float d = x - m[e];
-            const float ex = __builtin_amdgcn_exp2f(-fabsf(d));
             if (tc < nc[e]) {
-              s[e] = d > 0.f ? fmaf(s[e], ex, 1.f) : s[e] + ex;
-              m[e] = fmaxf(m[e], x);
+              const float mx = fmaxf(fmaxf(acc[0][e] * a.scale2, acc[1][e] * a.scale2), m[e]);
+              s[e] *= __builtin_amdgcn_exp2f(m[e] - mx);
+              m[e] = mx;
             }
           }
         }
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (tc < nc[e])
+            s[e] += __builtin_amdgcn_exp2f(fmaf(acc[0][e], a.scale2, -m[e])) +
+                    __builtin_amdgcn_exp2f(fmaf(acc[1][e], a.scale2, -m[e]));
       }
     }
     if (t + 1 < n_t) store(buf ^ 1);
@@ -252,28 +264,32 @@ __global__ __launch_bounds__(kTokThreads) void token_logits_kernel(TokArgs a) {
   }
 }
 
-// grid: ceil(Hkv * r_pad / 256). lse2[g][row] = M + log2(sum over chunks of s_k 2^(m_k - M)), the
-// chunks in order; +inf for rows without candidates (their weights are then 0).
+// grid: ceil(Hkv * r_pad / 4), one wave per row. lse2[g][row] = M + log2(sum over chunks of
+// s_k 2^(m_k - M)); lane l takes chunks l, l + 64, ... in order, and the 64 lane values are
+// combined by a fixed butterfly. +inf for rows without candidates (their weights are then 0).
 __global__ __launch_bounds__(256) void token_lse_kernel(const float2* __restrict__ stats, const ClusterGeo* __restrict__ geo,
                                                        int n_clusters, int group, int gp, int r_pad, int num_kv_heads,
                                                        int n_chunks, int chunk_tokens, float* __restrict__ lse2) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= num_kv_heads * r_pad) return;
+  const int idx = blockIdx.x * 4 + threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  if (idx >= num_kv_heads * r_pad) return;                 // uniform over the wave
   const int row = idx % r_pad;
   const int j = row / gp, i = row % gp;
-  float v = INFINITY;
-  if (j < n_clusters && i < group) {
-    const int used = (geo[j].n_cand + chunk_tokens - 1) / chunk_tokens;
-    if (used > 0) {
-      const float2* st = stats + (int64_t)idx * n_chunks;
-      float M = -INFINITY;
-      for (int k = 0; k < used; ++k) M = fmaxf(M, st[k].x);
-      float z = 0.f;
-      for (int k = 0; k < used; ++k) z += st[k].y * exp2f(st[k].x - M);
-      v = M + log2f(z);
-    }
+  const int used = (j < n_clusters && i < group) ? (geo[j].n_cand + chunk_tokens - 1) / chunk_tokens : 0;
+  if (used == 0) {
+    if (lane == 0) lse2[idx] = INFINITY;
+    return;
   }
-  lse2[idx] = v;
+  const float2* st = stats + (int64_t)idx * n_chunks;
+  float m = -INFINITY;
+  for (int k = lane; k < used; k += 64) m = fmaxf(m, st[k].x);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  float z = 0.f;
+  for (int k = lane; k < used; k += 64) z += st[k].y * exp2f(st[k].x - m);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) z += __shfl_xor(z, o, 64);
+  if (lane == 0) lse2[idx] = m + log2f(z);
 }
 
 // grid: (64-row tile of the selection, KV head, cluster). Copies rows [64 u, 64 u + 64) of
@@ -384,7 +400,7 @@ hipError_t launch_token_selection(const float* fingerprints, const uint16_t* k_p
   e = head_dim == 128 ? launch_logits_d<128, false>(p.gp, grid, a, stream) : launch_logits_d<64, false>(p.gp, grid, a, stream);
   if (e != hipSuccess) return e;
   const int n_rows = num_kv_heads * p.r_pad;
-  token_lse_kernel<<<(n_rows + 255) / 256, 256, 0, stream>>>(stats, geo, n_clusters, group, p.gp, p.r_pad,
+  token_lse_kernel<<<(n_rows + 3) / 4, 256, 0, stream>>>(stats, geo, n_clusters, group, p.gp, p.r_pad,
                                                               num_kv_heads, p.n_chunks, p.chunk_tokens, lse2);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return head_dim == 128 ? launch_logits_d<128, true>(p.gp, grid, a, stream) : launch_logits_d<64, true>(p.gp, grid, a, stream);

@@ -188,7 +188,8 @@ def check_token_scores(gpu_scores: np.ndarray, ref, bounds, block_size: int, wha
 def check_token_selection(gpu_sel, gpu_cnt, gpu_scores, ref, bounds, block_size: int, what: str):
     """The GPU selection is exactly the top-k of its own fp32 scores (score descending, position
     ascending); against the oracle scores it is valid to twice the bound, and equal to the oracle's
-    wherever the oracle's gap at the threshold exceeds four times the bound."""
+    wherever the bounds cannot reorder the threshold: every oracle-selected score minus its bound
+    above every unselected score plus its bound."""
     n_exact = 0
     for j, (g, s_ref, sc, bd) in enumerate(zip(ref["geometry"], ref["selections"], ref["scores"], bounds)):
         cnt = int(gpu_cnt[j])
@@ -208,13 +209,14 @@ def check_token_selection(gpu_sel, gpu_cnt, gpu_scores, ref, bounds, block_size:
         if cnt == 0:
             continue
         eps = 2 * float(bd.max())
-        srt = np.sort(sc)[::-1]
-        kth = srt[cnt - 1]
+        kth = np.sort(sc)[::-1][cnt - 1]
         chosen = np.zeros(g.n_cand, dtype=bool)
         chosen[got - first] = True
         assert np.all(sc[chosen] >= kth - eps), f"{what} cluster {j}: a selected token is not within eps of top-k"
         assert np.all(sc[~chosen] <= kth + eps), f"{what} cluster {j}: an unselected token beats the k-th by > eps"
-        if srt[cnt - 1] - srt[cnt] > 2 * eps:
+        in_ref = np.zeros(g.n_cand, dtype=bool)
+        in_ref[np.asarray(s_ref, dtype=np.int64) - first] = True
+        if (sc[in_ref] - bd[in_ref]).min() > (sc[~in_ref] + bd[~in_ref]).max():
             assert np.array_equal(got, s_ref), f"{what} cluster {j}: differs from the oracle above the margin"
             n_exact += 1
     return n_exact
