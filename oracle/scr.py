@@ -56,13 +56,13 @@ their reasons in the design notes:
   R25 incremental prefill (Sec. 3.1's outer-chunk loop): the clusters may cover only the last
       sub-chunks [cluster_start[0], M); the cache holds every earlier token, and rows before
       cluster_start[0] * L are not computed
-  R27 token-level selection (TokenSelect's granularity, Sec. 5.1.3): the candidates are the single
-      tokens between the sink blocks and the local window, each scored per head with its own key;
-      top_k counts tokens. Sinks and the local window keep their block rounding (R10, R11)
   R26 the overlap ratio (Eq. 7) compares the cluster's set I_C (anchor fingerprint, the cluster's
       candidates) with the union of the sets each member sub-chunk selects on its own, as the
       per-sub-chunk baseline would (its own fingerprint and its own candidate range, the
       single-sub-chunk geometry); it is undefined (NaN) when I_C is empty
+  R27 token-level selection (TokenSelect's granularity, Sec. 5.1.3): the candidates are the single
+      tokens between the sink blocks and the local window, each scored per head with its own key;
+      top_k counts tokens. Sinks and the local window keep their block rounding (R10, R11)
 """
 from __future__ import annotations
 
