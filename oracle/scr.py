@@ -63,6 +63,13 @@ their reasons in the design notes:
   R27 token-level selection (TokenSelect's granularity, Sec. 5.1.3): the candidates are the single
       tokens between the sink blocks and the local window, each scored per head with its own key;
       top_k counts tokens. Sinks and the local window keep their block rounding (R10, R11)
+  R28 bound representative keys (the query-aware page criticality of Quest, cited in Sec. 2): per
+      block and KV head the channel-wise minimum and maximum of the valid keys, and the logit
+      sigma * sum_i max(v_i mn_i, v_i mx_i), an upper bound of v . k over the block's keys (for
+      sigma > 0); it replaces R2's mean in block-level selection
+  R29 per-KV-head index sets: instead of R7's one set per cluster, every KV head g gets its own
+      top-k, voted by the softmax weights of its own query heads only; query head h attends over
+      the set of g(h)
 """
 from __future__ import annotations
 
@@ -79,9 +86,13 @@ __all__ = [
     "logical_rows",
     "selected_positions",
     "rep_keys",
+    "rep_bounds",
     "anchor_fingerprint",
     "block_logits",
+    "bound_logits",
     "soft_vote",
+    "soft_vote_groups",
+    "group_sets",
     "select_topk",
     "key_positions",
     "attention_rows",
@@ -186,6 +197,22 @@ def rep_keys(k_pages, block_table, n_tokens: int, block_size: int, blocks=None) 
     return out
 
 
+def rep_bounds(k_pages, block_table, n_tokens: int, block_size: int, blocks=None):
+    """R28: channel-wise minimum and maximum of K[t][g] over the valid tokens t of block b.
+    Returns (mn, mx), each [n, Hkv, d] fp64."""
+    n_blocks = -(-n_tokens // block_size)
+    blocks = np.arange(n_blocks) if blocks is None else np.asarray(blocks)
+    Hkv, d = k_pages.shape[1], k_pages.shape[3]
+    mn = np.empty((len(blocks), Hkv, d), dtype=np.float64)
+    mx = np.empty((len(blocks), Hkv, d), dtype=np.float64)
+    for i, b in enumerate(blocks):
+        n_valid = min(block_size, n_tokens - int(b) * block_size)
+        keys = bf16_to_f64(k_pages[int(block_table[int(b)]), :, :n_valid, :])   # [Hkv, n_valid, d]
+        mn[i] = keys.min(axis=1)
+        mx[i] = keys.max(axis=1)
+    return mn, mx
+
+
 def anchor_fingerprint(q, s: int, anchor_end: int) -> np.ndarray:
     """Eq. 6 on the anchor sub-chunk (Eq. 9): v[h] = mean over rows p in [s, anchor_end) of q[p][h].
 
@@ -206,6 +233,37 @@ def block_logits(v, k_rep_cand, num_kv_heads: int, score_scale: float = 1.0) -> 
         g = (h * num_kv_heads) // Hq
         x[h] = score_scale * (k_rep_cand[:, g, :] @ v[h])
     return x
+
+
+def bound_logits(v, mn_cand, mx_cand, num_kv_heads: int, score_scale: float = 1.0) -> np.ndarray:
+    """R28: x[h][b] = sigma * sum_i max(v[h][i] mn[b][g(h)][i], v[h][i] mx[b][g(h)][i]).
+
+    ``v`` [Hq, d]; ``mn_cand``, ``mx_cand`` [n_cand, Hkv, d]. Returns [Hq, n_cand].
+    """
+    Hq = v.shape[0]
+    x = np.empty((Hq, mn_cand.shape[0]), dtype=np.float64)
+    for h in range(Hq):
+        g = (h * num_kv_heads) // Hq
+        x[h] = score_scale * np.maximum(mn_cand[:, g, :] * v[h], mx_cand[:, g, :] * v[h]).sum(axis=1)
+    return x
+
+
+def soft_vote_groups(x, num_kv_heads: int) -> np.ndarray:
+    """R29: the soft-voting scores of each KV head's own query heads: [Hkv, n_cand]."""
+    Hq = x.shape[0]
+    G = Hq // num_kv_heads
+    return np.stack([soft_vote(x[g * G:(g + 1) * G]) for g in range(num_kv_heads)])
+
+
+def group_sets(sel, num_kv_heads: int) -> list:
+    """A selection as one index array per KV head: a 2-D [Hkv, cnt] array is one set per KV head
+    (R29); a 1-D array is one set shared by every head (R7)."""
+    a = np.asarray(sel, dtype=np.int64)
+    if a.ndim == 2:
+        if a.shape[0] != num_kv_heads:
+            raise ValueError("per-KV-head selection needs one row per KV head")
+        return [a[g] for g in range(num_kv_heads)]
+    return [a] * num_kv_heads
 
 
 def soft_vote(x) -> np.ndarray:
@@ -270,24 +328,35 @@ def attention_rows(q, k_pages, v_pages, block_table, geo: ClusterGeometry, sel, 
     if len(rows) == 0:
         return out
     # Logical keys/values of every position any requested row can see: the sink and selected
-    # sets (visible to every row) then the local window up to the last requested row.
+    # sets (visible to every row) then the local window up to the last requested row. With one
+    # set per KV head (R29) each KV head has its own selected positions.
     p_max = int(rows.max())
-    fixed = np.concatenate([np.arange(geo.sink_eff * B), selected_positions(geo, sel, B)])
-    pos = np.concatenate([fixed, np.arange(geo.lo_blk * B, p_max + 1)]).astype(np.int64)
-    Kx = logical_rows(k_pages, block_table, pos, B)      # [nk, Hkv, d]
-    Vx = logical_rows(v_pages, block_table, pos, B)
     qx = bf16_to_f64(q[rows])                            # [nr, Hq, d]
-    # Mask from the key-set definition: key t is visible to row p iff t is in Kset(p).
-    n_fixed = len(fixed)
-    visible = np.ones((len(rows), len(pos)), dtype=bool)
-    visible[:, n_fixed:] = pos[None, n_fixed:] <= rows[:, None]
+    sets = group_sets(sel, Hkv)
+    per_set = {}                                         # keyed by set: a shared set is read once
+
+    def keys_of(g):
+        key = id(sets[g])
+        if key not in per_set:
+            fixed = np.concatenate([np.arange(geo.sink_eff * B), selected_positions(geo, sets[g], B)])
+            pos = np.concatenate([fixed, np.arange(geo.lo_blk * B, p_max + 1)]).astype(np.int64)
+            # Mask from the key-set definition: key t is visible to row p iff t is in Kset(p).
+            n_fixed = len(fixed)
+            visible = np.ones((len(rows), len(pos)), dtype=bool)
+            visible[:, n_fixed:] = pos[None, n_fixed:] <= rows[:, None]
+            per_set[key] = (logical_rows(k_pages, block_table, pos, B), logical_rows(v_pages, block_table, pos, B),
+                            visible)
+        K, V, visible = per_set[key]
+        return K[:, g, :], V[:, g, :], visible
+
     for hi, h in enumerate(heads):
         g = (int(h) * Hkv) // Hq
-        s = (qx[:, h, :] @ Kx[:, g, :].T) * scale         # [nr, nk]
+        Kg, Vg, visible = keys_of(g)
+        s = (qx[:, h, :] @ Kg.T) * scale                    # [nr, nk]
         s = np.where(visible, s, -np.inf)
         m = s.max(axis=1, keepdims=True)
         w = np.exp(s - m)
-        out[:, hi, :] = (w @ Vx[:, g, :]) / w.sum(axis=1, keepdims=True)
+        out[:, hi, :] = (w @ Vg) / w.sum(axis=1, keepdims=True)
     return out
 
 
@@ -305,18 +374,26 @@ def cluster_attention(q, k_pages, v_pages, block_table, geo, sel, block_size, so
 def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, block_size: int,
             top_k: int, sink_tokens: int, local_window: int, cluster_start, score_scale: float = 1.0,
             softmax_scale: float | None = None, with_output: bool = True, external_sel=None,
-            select_tokens: bool = False) -> dict:
+            select_tokens: bool = False, rep_kind: str = "mean", kv_head_sets: bool = False) -> dict:
     """Algorithm 2 for one layer with a given cluster assignment.
 
     For each cluster: anchor fingerprint -> block logits -> soft-voting scores -> top-k
     (selection) -> attention of every row over sink + selected + local keys.
     ``external_sel`` (list of index arrays) replaces the oracle's own selection in the attention
     step, so attention can be checked under another selection.
+    ``rep_kind`` "minmax" scores blocks by the R28 bound; ``kv_head_sets`` gives every KV head its
+    own set (R29): a cluster's scores are then [Hkv, n_cand], its selection [Hkv, cnt] and its
+    margins [Hkv].
     Returns a dict with geometry, k_rep, fingerprints, scores, selections, margins, output.
     """
+    if rep_kind not in ("mean", "minmax"):
+        raise ValueError("rep_kind is 'mean' or 'minmax'")
+    if rep_kind == "minmax" and select_tokens:
+        raise ValueError("bound representative keys apply to block-level selection")
     geo = geometry(n_tokens, sub_chunk, block_size, sink_tokens, local_window, top_k, cluster_start,
                    select_tokens)
     k_rep = rep_keys(k_pages, block_table, n_tokens, block_size)
+    bounds = rep_bounds(k_pages, block_table, n_tokens, block_size) if rep_kind == "minmax" else None
     Hkv = k_pages.shape[1]
     B = block_size
     fps, scores, sels, margins = [], [], [], []
@@ -326,12 +403,22 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
             # R27: the candidates are single tokens, scored with their own keys
             cand = logical_rows(k_pages, block_table, np.arange(g.sink_blk * B, g.sink_blk * B + g.n_cand), B)
             first = g.sink_blk * B
-        else:
-            cand = k_rep[g.sink_blk:g.sink_blk + g.n_cand]
+            x = block_logits(v, cand, Hkv, score_scale)
+        elif rep_kind == "minmax":
+            c = slice(g.sink_blk, g.sink_blk + g.n_cand)
             first = g.sink_blk
-        x = block_logits(v, cand, Hkv, score_scale)
-        sc = soft_vote(x)
-        sel, margin = select_topk(sc, first, top_k)
+            x = bound_logits(v, bounds[0][c], bounds[1][c], Hkv, score_scale)
+        else:
+            first = g.sink_blk
+            x = block_logits(v, k_rep[g.sink_blk:g.sink_blk + g.n_cand], Hkv, score_scale)
+        if kv_head_sets:
+            sc = soft_vote_groups(x, Hkv) if x.shape[1] else np.zeros((Hkv, 0))
+            picks = [select_topk(sc[kv], first, top_k) for kv in range(Hkv)]
+            sel = np.stack([p[0] for p in picks]) if picks else np.zeros((Hkv, 0), dtype=np.int64)
+            margin = np.array([p[1] for p in picks])
+        else:
+            sc = soft_vote(x)
+            sel, margin = select_topk(sc, first, top_k)
         fps.append(v)
         scores.append(sc)
         sels.append(sel)
@@ -346,6 +433,7 @@ def prefill(q, k_pages, v_pages, block_table, n_tokens: int, *, sub_chunk: int, 
     return {
         "geometry": geo,
         "k_rep": k_rep,
+        "bounds": bounds,
         "fingerprints": fps,
         "scores": scores,
         "selections": sels,

@@ -180,3 +180,61 @@ def brute_prefill_tokens(q_bits, k_pages, v_pages, block_table, n_tokens, L, B, 
                 vis[p, t] = True
     return {"layout": layout, "scores": scores, "selections": sels, "mask": vis,
             "output": masked_attention(q, K, V, vis)}
+
+
+def brute_prefill_variants(q_bits, k_pages, v_pages, block_table, n_tokens, L, B, S, W, k, cluster_start,
+                           score_scale=1.0, bounds=False, per_kv_head=False):
+    """Block-level selection with the two variants by explicit loops.
+
+    bounds: a block's logit for head h is sigma * sum over channels i of the larger of v_i * lo_i
+    and v_i * hi_i, lo_i / hi_i the smallest / largest channel-i key value among the block's tokens
+    (found by scanning the tokens), v the anchor-row mean (summed row by row).
+    per_kv_head: the softmax weights are summed over the query heads of each KV head separately;
+    every KV head picks its own best-total k-subset and its query heads attend under its own mask.
+    """
+    q = widen(q_bits)
+    K = unpage(k_pages, block_table)
+    V = unpage(v_pages, block_table)
+    Hkv = k_pages.shape[1]
+    Hq, d = q.shape[1], q.shape[2]
+    G = Hq // Hkv
+    layout = cluster_layout(n_tokens, L, B, S, W, cluster_start)
+    groups = list(range(Hkv)) if per_kv_head else [None]
+    sels = {gr: [] for gr in groups}
+    for (s, e, a_end, lo_blk, sink_eff, cand) in layout:
+        totals = {gr: {b: 0.0 for b in cand} for gr in groups}
+        for h in range(Hq):
+            g = h // G
+            v = [0.0] * d
+            for p in range(s, a_end):
+                for i in range(d):
+                    v[i] += q[p, h, i]
+            v = [x / (a_end - s) for x in v]
+            logits = {}
+            for b in cand:
+                if bounds:
+                    acc = 0.0
+                    for i in range(d):
+                        lo_i = min(K[t, g, i] for t in range(b * B, (b + 1) * B))
+                        hi_i = max(K[t, g, i] for t in range(b * B, (b + 1) * B))
+                        acc += max(v[i] * lo_i, v[i] * hi_i)
+                    logits[b] = score_scale * acc
+                else:
+                    logits[b] = score_scale * sum(float(np.dot(K[t, g, :], v)) for t in range(b * B, (b + 1) * B)) / B
+            if not logits:
+                continue
+            mx = max(logits.values())
+            den = sum(math.exp(x - mx) for x in logits.values())
+            gr = g if per_kv_head else None
+            for b in cand:
+                totals[gr][b] += math.exp(logits[b] - mx) / den
+        for gr in groups:
+            sels[gr].append(brute_select(totals[gr], k))
+    out = np.empty_like(q)
+    for gr in groups:
+        vis = visibility_mask(n_tokens, layout, sels[gr], B)
+        full = masked_attention(q, K, V, vis)
+        heads = range(Hq) if gr is None else range(gr * G, (gr + 1) * G)
+        for h in heads:
+            out[:, h, :] = full[:, h, :]
+    return {"layout": layout, "selections": sels, "output": out}
