@@ -13,8 +13,9 @@ Prints ONE JSON line (rank 0) with the throughput, the roofline of the dominant 
 oracle timed on a bounded sample on the host's cores.
 
 Other modes (one JSON line each, no CPU baseline unless stated): --sweep over cluster sizes,
---theta / --theta-sweep with clusters formed on the GPU by anchor-based clustering, and
---tokens K for token-level selection with a budget of K tokens.
+--theta / --theta-sweep with clusters formed on the GPU by anchor-based clustering, --tokens K
+for token-level selection with a budget of K tokens, and the selection variants --rep-bounds,
+--kv-sets and --score-scale.
 """
 from __future__ import annotations
 
@@ -51,6 +52,10 @@ def parse_args():
                     help="also report the top-k overlap ratio (Eq. 7) of the clusters against per-sub-chunk selection")
     ap.add_argument("--tokens", type=int, default=0,
                     help="token-level selection with this budget in tokens (0: block-level selection)")
+    ap.add_argument("--rep-bounds", action="store_true",
+                    help="score blocks by their channel-wise key bounds (min / max) instead of the mean key")
+    ap.add_argument("--kv-sets", action="store_true", help="one selected set per (cluster, KV head)")
+    ap.add_argument("--score-scale", type=float, default=0.0, help="selection logit scale sigma (0: 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
     ap.add_argument("--out-bf16", action="store_true")
@@ -81,7 +86,7 @@ def measured_traffic(workload_name):
     return int(block["traffic_bytes"])
 
 
-def geometry_work(w, geo, tokens=False):
+def geometry_work(w, geo, tokens=False, bounds=False):
     """Algorithmic attention FLOPs and the selection-side bytes from the cluster geometry.
 
     Attention: 4 d Hq per (query row, visible key) pair (two products of 2 d FLOP), over
@@ -112,12 +117,13 @@ def geometry_work(w, geo, tokens=False):
             "vote_bytes": n_cand * Hkv * 4,
             "gather_bytes": 2 * 2 * n_sel * Hkv * d * 2,
         }
+    rep = 2 if bounds else 1        # bound form: channel-wise minimum and maximum per block
     return {
         "attention_flops": 4.0 * d * Hq * pairs,
         "pairs": pairs,
-        "rep_keys_bytes": w.n_tokens * Hkv * d * 2 + nb * Hkv * d * 4,
+        "rep_keys_bytes": w.n_tokens * Hkv * d * 2 + rep * nb * Hkv * d * 4,
         "fingerprint_bytes": anchor_rows * Hq * d * 2 + n_clusters * Hq * d * 4,
-        "logits_bytes": n_cand * Hkv * d * 4 + n_cand * Hq * 4 + n_clusters * Hq * d * 4,
+        "logits_bytes": rep * n_cand * Hkv * d * 4 + n_cand * Hq * 4 + n_clusters * Hq * d * 4,
         "vote_bytes": n_cand * Hq * 4,
     }
 
@@ -202,7 +208,8 @@ def time_path(args, w, c, layers, dev, theta=None):
     cfg = pk.config_for(num_q_heads=w.num_q_heads, num_kv_heads=w.num_kv_heads, head_dim=w.head_dim,
                         block_size=w.block_size, sub_chunk=w.sub_chunk, top_k=args.tokens if tokens else w.top_k,
                         sink_tokens=w.sink_tokens, local_window=w.local_window, max_tokens=w.n_tokens,
-                        max_clusters=max_clusters, out_bf16=args.out_bf16, select_tokens=tokens)
+                        max_clusters=max_clusters, out_bf16=args.out_bf16, select_tokens=tokens,
+                        rep_bounds=args.rep_bounds, kv_head_sets=args.kv_sets, score_scale=args.score_scale)
     h = pk.Scale(cfg)
     if theta is None:
         cs = gen.cluster_starts(w.n_sub_chunks, c)
@@ -211,7 +218,7 @@ def time_path(args, w, c, layers, dev, theta=None):
         layer_cs = [h.cluster_subchunks(q, w.n_tokens, theta, l_max, args.outer) for q, *_ in layers]
         cs = layer_cs[0]
     geo = pk.scale_cluster_geometry(cfg, w.n_tokens, cs)
-    work = geometry_work(w, geo, tokens)
+    work = geometry_work(w, geo, tokens, bounds=args.rep_bounds)
     # one set of outputs shared by the layers: each layer's output is complete when its attention
     # call ends, and the next layer's calls are ordered after it on the stream
     bufs = pk.LayerBuffers(cfg, w.n_tokens, max_clusters, device=dev)
@@ -243,7 +250,7 @@ def time_path(args, w, c, layers, dev, theta=None):
     t1 = time.perf_counter()
     stages = h.stage_times(reset=True)
     calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
-    overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap and not tokens else None
+    overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap and not tokens and not args.kv_sets else None
     h.close()
     del bufs
 
@@ -303,6 +310,9 @@ def time_path(args, w, c, layers, dev, theta=None):
             "sub_chunk": w.sub_chunk, "cluster": c if theta is None else f"anchor clustering, theta {theta}",
             "top_k": w.top_k if not tokens else None,
             "select_tokens": args.tokens if tokens else None, "sink_tokens": w.sink_tokens,
+            "rep_keys": "channel-wise bounds" if args.rep_bounds else "mean",
+            "index_sets": "per KV head" if args.kv_sets else "per cluster",
+            "score_scale": args.score_scale or 1.0,
             "local_window": w.local_window, "out_dtype": "bf16" if args.out_bf16 else "fp32",
             "seed": w.seed,
         },
@@ -313,8 +323,8 @@ def time_path(args, w, c, layers, dev, theta=None):
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": (measured_traffic(w.name) if theta is None and not tokens and c == gen.WORKLOADS[w.name].cluster
-                        else None),
+            "traffic": (measured_traffic(w.name) if theta is None and not tokens and not args.kv_sets
+                        and c == gen.WORKLOADS[w.name].cluster else None),
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
         },
@@ -425,7 +435,8 @@ def main():
         wc = w.with_(cluster=c)
         print(f"[bench] timing " + (f"theta={theta}" if theta is not None else f"c={c}"), file=sys.stderr, flush=True)
         result, cs, geo = time_path(args, wc, c, layers, dev, theta=theta)
-        if rank == 0 and not args.no_cpu_baseline and not args.tokens:
+        variant = args.tokens or args.rep_bounds or args.kv_sets or args.score_scale
+        if rank == 0 and not args.no_cpu_baseline and not variant:
             print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
             result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles)
         if rank == 0:

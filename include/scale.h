@@ -35,9 +35,12 @@
  *    k_pages bf16  [n_pages][Hkv][B][d]   paged key cache, one page = one block of B tokens
  *    v_pages bf16  [n_pages][Hkv][B][d]   paged value cache, same paging as k_pages
  *    block_table int32 [nb]               page holding logical block b; NULL = identity
- *    k_rep   fp32  [nb][Hkv][d]           representative keys
+ *    k_rep   fp32  [nb][Hkv][d]           representative keys ([nb][Hkv][2][d]: channel-wise
+ *                                         minimum, then maximum, with rep_kind = SCALE_REP_BOUNDS)
  *    sel_idx int32 [n_clusters][top_k]    selected blocks per cluster, ascending, -1 padded
+ *                                         ([n_clusters][Hkv][top_k] with kv_head_sets = 1)
  *    sel_cnt int32 [n_clusters]           number of valid entries of each sel_idx row
+ *                                         ([n_clusters][Hkv] with kv_head_sets = 1)
  *    out     fp32 or bf16 [N][Hq][d]      attention output (config.out_dtype)
  * Query head h reads KV head floor(h * Hkv / Hq) (consecutive query heads share a KV head).
  *
@@ -76,6 +79,14 @@ typedef enum {
 
 typedef enum { SCALE_OUT_F32 = 0, SCALE_OUT_BF16 = 1 } scale_out_dtype;
 
+/* How a KV block is summarised for block-level selection. */
+typedef enum {
+  SCALE_REP_MEAN = 0,   /* the mean key; logit sigma * v . mean                                    */
+  SCALE_REP_BOUNDS = 1  /* channel-wise min / max of the block's keys (the page criticality of
+                           Quest, cited in the paper's Sec. 2); logit sigma * sum_i max(v_i mn_i,
+                           v_i mx_i), an upper bound of v . k over the block for sigma > 0          */
+} scale_rep_kind;
+
 typedef struct {
   int32_t num_q_heads;   /* Hq >= 1, a multiple of num_kv_heads                              */
   int32_t num_kv_heads;  /* Hkv >= 1                                                         */
@@ -93,6 +104,13 @@ typedef struct {
   int32_t out_dtype;     /* scale_out_dtype of the attention output                          */
   int32_t select_tokens; /* 0: block-level selection; 1: token-level selection (top_k counts
                             tokens; scale_init also allocates the token calls' scratch)      */
+  int32_t rep_kind;      /* scale_rep_kind of block-level selection (SCALE_REP_BOUNDS with
+                            select_tokens = 1 is SCALE_ERR_UNSUPPORTED)                      */
+  int32_t kv_head_sets;  /* 0: one selected set per cluster, voted by every query head (Sec.
+                            5.1.3 head soft-voting); 1: one set per (cluster, KV head), voted by
+                            that KV head's query heads only, and query head h attends over the
+                            set of its KV head (sel_idx, sel_cnt and scores_out gain a KV-head
+                            dimension)                                                         */
 } scale_config;
 
 /* Create a handle bound to the current HIP device and to `hip_stream` (a hipStream_t; NULL is
@@ -134,6 +152,10 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens / B]; candidate entries
  *   receive their score, every other entry -1.
  * fingerprints_out (optional, may be NULL): device fp32 [n_clusters][Hq][d] anchor fingerprints.
+ * With rep_kind = SCALE_REP_BOUNDS, k_rep holds the channel-wise bounds and x[h][b] = score_scale *
+ * sum_i max(v[h][i] mn[b][g(h)][i], v[h][i] mx[b][g(h)][i]). With kv_head_sets = 1, score and top-k
+ * are taken per (cluster j, KV head g) over the query heads of g only, into row j * Hkv + g of
+ * sel_idx, sel_cnt and scores_out.
  * Each call adds n_clusters to the handle's retrieval-call counter. On a select_tokens handle
  * this call returns SCALE_ERR_UNSUPPORTED (use scale_select_cluster_tokens). */
 scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens,
@@ -154,6 +176,7 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
  * cluster_start, sel_cnt and fingerprints_out as for scale_select_cluster.
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens]; candidate entries
  *   receive their score, every other entry -1.
+ * kv_head_sets = 1 works as for scale_select_cluster (rows j * Hkv + g).
  * Each call adds n_clusters to the handle's retrieval-call counter. */
 scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens,
                                          const uint16_t* k_pages, const int32_t* block_table,
@@ -170,7 +193,8 @@ scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int3
  * the selection. bf16 output is the round-to-nearest-even of the fp32 result.
  * On a select_tokens handle, sel_idx rows hold token positions (as scale_select_cluster_tokens
  * writes them; each is clamped to [0, n_tokens)) and Kset(p) = sink blocks U those tokens U tokens
- * [lo_blk * B, p]; the selected keys and values are first gathered into handle scratch. */
+ * [lo_blk * B, p]; the selected keys and values are first gathered into handle scratch.
+ * With kv_head_sets = 1, query head h of cluster j uses selection row j * Hkv + g(h). */
 scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint16_t* k_pages,
                                   const uint16_t* v_pages, const int32_t* block_table,
                                   int32_t n_tokens, const int32_t* cluster_start,

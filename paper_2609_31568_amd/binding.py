@@ -22,6 +22,8 @@ SCALE_ERR_CAPACITY = -4
 SCALE_ERR_HIP = -5
 SCALE_OUT_F32 = 0
 SCALE_OUT_BF16 = 1
+SCALE_REP_MEAN = 0
+SCALE_REP_BOUNDS = 1
 
 EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
@@ -53,6 +55,8 @@ class scale_config(ctypes.Structure):
         ("score_scale", ctypes.c_float),
         ("out_dtype", ctypes.c_int32),
         ("select_tokens", ctypes.c_int32),
+        ("rep_kind", ctypes.c_int32),
+        ("kv_head_sets", ctypes.c_int32),
     ]
 
 
@@ -120,10 +124,11 @@ def _cluster_start(cs) -> np.ndarray:
 
 def make_config(*, num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
                 local_window, max_tokens, max_clusters, softmax_scale=0.0, score_scale=0.0,
-                out_dtype=SCALE_OUT_F32, select_tokens=False) -> scale_config:
+                out_dtype=SCALE_OUT_F32, select_tokens=False, rep_kind=SCALE_REP_MEAN,
+                kv_head_sets=False) -> scale_config:
     return scale_config(num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
                         local_window, max_tokens, max_clusters, softmax_scale, score_scale, out_dtype,
-                        1 if select_tokens else 0)
+                        1 if select_tokens else 0, int(rep_kind), 1 if kv_head_sets else 0)
 
 
 def scale_cluster_geometry(cfg: scale_config, n_tokens: int, cluster_start) -> np.ndarray:

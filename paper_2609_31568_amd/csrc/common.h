@@ -30,10 +30,11 @@ static_assert(sizeof(WorkItem) == 16, "WorkItem is uploaded as raw bytes");
 
 // ---- launchers (each defined next to its kernel) ----
 
-// k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32), for the
-// logical blocks b in [first_block, n_blocks).
+// k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32), or with
+// `bounds` k_rep[b][g][0 / 1][:] = its channel-wise minimum / maximum, for the logical blocks b in
+// [first_block, n_blocks).
 hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, int first_block, int n_blocks,
-                           int num_kv_heads, int block_size, int head_dim, float* k_rep,
+                           int num_kv_heads, int block_size, int head_dim, bool bounds, float* k_rep,
                            hipStream_t stream);
 
 // Anchor fingerprints: fp32 mean of each cluster's anchor rows (fp64 sums).
@@ -45,17 +46,18 @@ hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_c
 int selection_chunks(int max_cand);
 
 // Selection logits x[j][h][c] for candidate c of cluster j (row stride `cand_stride`), and each
-// candidate chunk's softmax partials per head.
+// candidate chunk's softmax partials per head; `bounds` scores the channel-wise key bounds.
 hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
                                int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                               int num_q_heads, int num_kv_heads, int head_dim, float score_scale,
+                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, float score_scale,
                                float* logits, float2* head_stats, hipStream_t stream);
 
-// Soft-voting scores and deterministic top-k per cluster.
+// Soft-voting scores and deterministic top-k per cluster, or per (cluster, KV head) with
+// `per_kv` (output rows j * Hkv + g, each voted by the query heads of g).
 hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo,
                             int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                            int num_q_heads, int top_k, int n_blocks, float* spill,
-                            int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                            int num_q_heads, int num_kv_heads, bool per_kv, int top_k, int n_blocks,
+                            float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                             hipStream_t stream);
 
 // Sub-chunk similarity for the anchor-based clustering of sub-chunks [first, M), M =
@@ -88,29 +90,29 @@ hipError_t launch_token_selection(const float* fingerprints, const uint16_t* k_p
                                   float score_scale, int64_t cand_stride, uint16_t* F, float2* stats, float* lse2,
                                   float* partial, hipStream_t stream);
 
-// Score = sum of the partials over KV heads (into spill [cluster][cand_stride]), then the
-// deterministic top-k of vote_topk; entries are token positions first_token + c. scores_out
-// (optional) rows have n_tokens entries.
+// Score = sum of the partials over KV heads (into spill [cluster][cand_stride]), or with `per_kv`
+// each KV head's own partial row, then the deterministic top-k of vote_topk; entries are token
+// positions first_token + c. scores_out (optional) rows have n_tokens entries.
 hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
-                                   int max_cand, int first_token, int num_kv_heads, int top_k, int n_tokens,
-                                   float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                   int max_cand, int first_token, int num_kv_heads, bool per_kv, int top_k,
+                                   int n_tokens, float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                                    hipStream_t stream);
 
 // Selected keys and values of every cluster copied to gk / gv [cluster][Hkv][kpad][d] in selection
 // order, kpad = top_k rounded up to kTokenTile; the rows of the last partial tile past sel_cnt are
 // zero.
 hipError_t launch_gather_selected(const uint16_t* k_pages, const uint16_t* v_pages, const int32_t* block_table,
-                                  const int32_t* sel_idx, const int32_t* sel_cnt, int n_clusters, int top_k,
-                                  int kpad, int n_tokens, int num_kv_heads, int head_dim, int block_size,
+                                  const int32_t* sel_idx, const int32_t* sel_cnt, bool per_kv, int n_clusters,
+                                  int top_k, int kpad, int n_tokens, int num_kv_heads, int head_dim, int block_size,
                                   uint16_t* gk, uint16_t* gv, hipStream_t stream);
 
 // Block-sparse attention over the work list. With gk != null (token-level selection) the selected
-// keys are the gathered rows gk / gv [cluster][Hkv][kpad][d], sel_cnt[j] of them, instead of the
-// blocks sel_idx names.
+// keys are the gathered rows gk / gv [cluster][Hkv][kpad][d], sel_cnt of them, instead of the
+// blocks sel_idx names. With `per_kv` the selection row of (cluster j, KV head g) is j * Hkv + g.
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
                                    const WorkItem* items, int n_items, const int32_t* sel_idx,
-                                   const int32_t* sel_cnt, int top_k, int num_q_heads,
+                                   const int32_t* sel_cnt, bool per_kv, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
                                    const uint16_t* gv, int kpad, hipStream_t stream);

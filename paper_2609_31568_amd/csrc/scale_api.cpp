@@ -93,6 +93,9 @@ scale_status validate_config(const scale_config* c) {
   if (!std::isfinite(c->score_scale)) return SCALE_ERR_INVALID_ARG;
   if (c->out_dtype != SCALE_OUT_F32 && c->out_dtype != SCALE_OUT_BF16) return SCALE_ERR_INVALID_ARG;
   if (c->select_tokens != 0 && c->select_tokens != 1) return SCALE_ERR_INVALID_ARG;
+  if (c->rep_kind != SCALE_REP_MEAN && c->rep_kind != SCALE_REP_BOUNDS) return SCALE_ERR_INVALID_ARG;
+  if (c->kv_head_sets != 0 && c->kv_head_sets != 1) return SCALE_ERR_INVALID_ARG;
+  if (c->select_tokens && c->rep_kind == SCALE_REP_BOUNDS) return SCALE_ERR_UNSUPPORTED;   // tokens use their keys
   if (c->head_dim != 64 && c->head_dim != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->block_size != 64 && c->block_size != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->sub_chunk % c->block_size) return SCALE_ERR_UNSUPPORTED;
@@ -284,7 +287,8 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
             dev((void**)&h->d_head_stats, sizeof(float2) * mc * c.num_q_heads * scale::selection_chunks(h->max_blocks)) &&
             dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
             dev((void**)&h->d_logits, sizeof(float) * mc * c.num_q_heads * (int64_t)h->max_blocks) &&
-            dev((void**)&h->d_spill, h->max_blocks > 8192 ? sizeof(float) * mc * h->max_blocks : 0) &&
+            dev((void**)&h->d_spill,
+                h->max_blocks > 8192 ? sizeof(float) * mc * (c.kv_head_sets ? c.num_kv_heads : 1) * h->max_blocks : 0) &&
             dev((void**)&h->d_sub_fp, sizeof(double) * (size_t)h->max_subchunks * row_elems) &&
             dev((void**)&h->d_inv_norm, sizeof(double) * (size_t)h->max_subchunks) &&
             dev((void**)&h->d_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan) &&
@@ -340,7 +344,8 @@ scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
   stage_begin(h);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, 0, n_tokens / c.block_size, c.num_kv_heads,
-                                              c.block_size, c.head_dim, k_rep, h->stream);
+                                              c.block_size, c.head_dim, c.rep_kind == SCALE_REP_BOUNDS, k_rep,
+                                              h->stream);
   stage_end(h, SCALE_STAGE_REP_KEYS);
   return check_launch(e);
 }
@@ -354,7 +359,8 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
   if (first_block > n_tokens / c.block_size) return SCALE_ERR_INVALID_ARG;
   stage_begin(h);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, first_block, n_tokens / c.block_size,
-                                              c.num_kv_heads, c.block_size, c.head_dim, k_rep, h->stream);
+                                              c.num_kv_heads, c.block_size, c.head_dim, c.rep_kind == SCALE_REP_BOUNDS,
+                                              k_rep, h->stream);
   stage_end(h, SCALE_STAGE_REP_KEYS);
   return check_launch(e);
 }
@@ -386,13 +392,15 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
   if (st != SCALE_OK) return st;
   stage_begin(h);
   st = check_launch(scale::launch_block_logits(fps, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
-                                               c.num_q_heads, c.num_kv_heads, c.head_dim, sigma, h->d_logits,
-                                               h->d_head_stats, h->stream));
+                                               c.num_q_heads, c.num_kv_heads, c.head_dim,
+                                               c.rep_kind == SCALE_REP_BOUNDS, sigma, h->d_logits, h->d_head_stats,
+                                               h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
   stage_begin(h);
-  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_head_stats, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
-                                            c.num_q_heads, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
+  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_head_stats, h->d_geo, n_clusters, max_cand,
+                                            h->max_blocks, sink_blk, c.num_q_heads, c.num_kv_heads,
+                                            c.kv_head_sets != 0, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
                                             scores_out, h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
@@ -434,8 +442,9 @@ scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int3
   if (st != SCALE_OK) return st;
   stage_begin(h);
   st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, c.max_tokens, max_cand,
-                                                   first_token, c.num_kv_heads, c.top_k, n_tokens, h->d_tok_score,
-                                                   sel_idx, sel_cnt, scores_out, h->stream));
+                                                   first_token, c.num_kv_heads, c.kv_head_sets != 0, c.top_k,
+                                                   n_tokens, h->d_tok_score, sel_idx, sel_cnt, scores_out,
+                                                   h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
   h->retrieval_calls += n_clusters;
@@ -550,17 +559,18 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   const bool tokens = c.select_tokens && h->kpad > 0;
   if (tokens) {
     stage_begin(h);
-    st = check_launch(scale::launch_gather_selected(k_pages, v_pages, block_table, sel_idx, sel_cnt, n_clusters,
-                                                    c.top_k, h->kpad, n_tokens, c.num_kv_heads, c.head_dim, B,
-                                                    h->d_gk, h->d_gv, h->stream));
+    st = check_launch(scale::launch_gather_selected(k_pages, v_pages, block_table, sel_idx, sel_cnt,
+                                                    c.kv_head_sets != 0, n_clusters, c.top_k, h->kpad, n_tokens,
+                                                    c.num_kv_heads, c.head_dim, B, h->d_gk, h->d_gv, h->stream));
     stage_end(h, SCALE_STAGE_GATHER);
     if (st != SCALE_OK) return st;
   }
   stage_begin(h);
   const hipError_t e = scale::launch_sparse_attention(
-      q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, c.top_k,
-      c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2, c.out_dtype == SCALE_OUT_BF16, out,
-      tokens ? h->d_gk : nullptr, tokens ? h->d_gv : nullptr, h->kpad, h->stream);
+      q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, c.kv_head_sets != 0,
+      c.top_k, c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
+      c.out_dtype == SCALE_OUT_BF16, out, tokens ? h->d_gk : nullptr, tokens ? h->d_gv : nullptr, h->kpad,
+      h->stream);
   stage_end(h, SCALE_STAGE_ATTENTION);
   return check_launch(e);
 }

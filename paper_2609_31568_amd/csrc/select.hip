@@ -4,8 +4,9 @@
 //
 //  fingerprint   (column slice, cluster) -> fp32 mean of the anchor rows (fp64 sums)
 //  block_logits  (cluster, candidate chunks, KV head) -> x[h][c] = sigma * v[h] . k_rep[c][g(h)]
-//                for the query heads h of KV head g, plus each chunk's softmax partials
-//                (max_c x[h][c], sum_c exp(x[h][c] - max)) per head
+//                for the query heads h of KV head g (bound form: sigma * sum_i max(v_i mn_i,
+//                v_i mx_i) over the block's channel-wise key bounds), plus each chunk's softmax
+//                partials (max_c x[h][c], sum_c exp(x[h][c] - max)) per head
 //  vote_topk     cluster -> per-head softmax normaliser from the chunk partials, score = sum over
 //                heads of the softmax weights, top-k by (score desc, block index asc), ascending
 //
@@ -83,7 +84,7 @@ __global__ __launch_bounds__(kFpThreads) void fingerprint_kernel(const uint16_t*
 // candidate's representative key (64 contiguous bytes per candidate per load), forms partial dot
 // products with the fingerprints of the (at most 8) query heads of g held in LDS, and the four
 // lanes add their partials.
-template <int D>
+template <int D, bool kBounds>
 __global__ __launch_bounds__(kThreads) void block_logits_kernel(
     const float* __restrict__ fingerprints, const float* __restrict__ k_rep,
     const ClusterGeo* __restrict__ geo, int parts, int n_chunks, int cand_stride, int sink_blk,
@@ -108,10 +109,15 @@ __global__ __launch_bounds__(kThreads) void block_logits_kernel(
   for (int chunk = p; chunk < chunks; chunk += parts) {
     const int c = chunk * kCandChunk + wave * 16 + lane / 4;
     const bool valid = c < G.n_cand;
-    float4 kv[kVec];
-    const float4* kr = reinterpret_cast<const float4*>(k_rep + ((int64_t)(sink_blk + (valid ? c : 0)) * num_kv_heads + g) * D);
+    float4 kv[kVec], kx[kBounds ? kVec : 1];
+    const float4* kr = reinterpret_cast<const float4*>(
+        k_rep + ((int64_t)(sink_blk + (valid ? c : 0)) * num_kv_heads + g) * (kBounds ? 2 * D : D));
 #pragma unroll
-    for (int i = 0; i < kVec; ++i) kv[i] = kr[4 * i + q4];
+    for (int i = 0; i < kVec; ++i) kv[i] = kr[4 * i + q4];               // mean, or the minima
+    if constexpr (kBounds) {
+#pragma unroll
+      for (int i = 0; i < kVec; ++i) kx[i] = kr[D / 4 + 4 * i + q4];    // the maxima
+    }
     float x[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -121,10 +127,17 @@ __global__ __launch_bounds__(kThreads) void block_logits_kernel(
 #pragma unroll
         for (int i = 0; i < kVec; ++i) {
           const float4 v = v_lds[u * (D / 4) + 4 * i + q4];
-          acc = fmaf(v.x, kv[i].x, acc);
-          acc = fmaf(v.y, kv[i].y, acc);
-          acc = fmaf(v.z, kv[i].z, acc);
-          acc = fmaf(v.w, kv[i].w, acc);
+          if constexpr (kBounds) {
+            acc += fmaxf(v.x * kv[i].x, v.x * kx[i].x);
+            acc += fmaxf(v.y * kv[i].y, v.y * kx[i].y);
+            acc += fmaxf(v.z * kv[i].z, v.z * kx[i].z);
+            acc += fmaxf(v.w * kv[i].w, v.w * kx[i].w);
+          } else {
+            acc = fmaf(v.x, kv[i].x, acc);
+            acc = fmaf(v.y, kv[i].y, acc);
+            acc = fmaf(v.z, kv[i].z, acc);
+            acc = fmaf(v.w, kv[i].w, acc);
+          }
         }
         acc += __shfl_xor(acc, 1, 64);
         acc += __shfl_xor(acc, 2, 64);
@@ -193,7 +206,8 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
   return before + incl - v;
 }
 
-// grid: cluster.
+// grid: output row = cluster, or (cluster, KV head) with one set per KV head (row j * Hkv + g,
+// voted by the query heads of g only).
 //  1. soft-voting: each head's softmax maximum and normaliser over all candidates, combined from
 //     the chunk partials in chunk order; then per candidate the sum over heads, in head order.
 //     Token mode (kTok): the per-KV-head partial sums of the token scoring kernel are added in
@@ -214,7 +228,8 @@ struct VoteArgs {
   int64_t cand_stride;
   int first;                   // index of candidate 0 (sink_blk, or sink_blk * B for tokens)
   int n_out;                   // row length of scores_out
-  float* spill;                // [cluster][cand_stride]
+  int per_kv;                  // 1: one set per (cluster, KV head), voted by its own query heads
+  float* spill;                // [output row][cand_stride]
   int32_t *sel_idx, *sel_cnt;
   float* scores_out;
 };
@@ -226,22 +241,29 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   __shared__ unsigned hist[kHistBins];
   __shared__ int pick[2];
   extern __shared__ float head_lds[];               // [Hq] maxima, then [Hq] 1 / normaliser
-  const int j = blockIdx.x;
+  const int row = blockIdx.x;
+  const int sets = a.per_kv ? a.num_kv_heads : 1;
+  const int j = row / sets;
   const ClusterGeo G = a.geo[j];
   const int n = G.n_cand;
   const int cnt = G.sel_cnt;
   const int top_k = a.top_k;
-  float* score = n <= kMaxLdsCand ? score_lds : a.spill + (int64_t)j * a.cand_stride;
+  float* score = n <= kMaxLdsCand ? score_lds : a.spill + (int64_t)row * a.cand_stride;
 
   // 1.
   if constexpr (kTok) {
-    score = a.spill + (int64_t)j * a.cand_stride;   // written by token_sum_kernel
+    // the KV head's own partial row, or the sum over KV heads written by token_sum_kernel
+    score = a.per_kv ? const_cast<float*>(a.partial) + (int64_t)row * a.cand_stride
+                     : a.spill + (int64_t)j * a.cand_stride;
   } else {
     const int num_q_heads = a.num_q_heads;
+    const int group = num_q_heads / a.num_kv_heads;
+    const int h0 = a.per_kv ? (row % sets) * group : 0;
+    const int h1 = a.per_kv ? h0 + group : num_q_heads;
     const int64_t cand_stride = a.cand_stride;
     const float* x = a.logits + (int64_t)j * num_q_heads * cand_stride;
     const int used = (n + kCandChunk - 1) / kCandChunk;
-    for (int h = threadIdx.x; h < num_q_heads; h += kVoteThreads) {
+    for (int h = h0 + (int)threadIdx.x; h < h1; h += kVoteThreads) {
       const float2* st = a.head_stats + ((int64_t)j * num_q_heads + h) * a.n_chunks;
       float m = -FLT_MAX;
       for (int k = 0; k < used; ++k) m = fmaxf(m, st[k].x);
@@ -253,29 +275,29 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
     __syncthreads();
     for (int c = threadIdx.x; c < n; c += kVoteThreads) {
       float acc = 0.f;
-      int h = 0;
-      for (; h + 16 <= num_q_heads; h += 16) {
+      int h = h0;
+      for (; h + 16 <= h1; h += 16) {
         float xv[16];
 #pragma unroll
         for (int u = 0; u < 16; ++u) xv[u] = x[(int64_t)(h + u) * cand_stride + c];
 #pragma unroll
         for (int u = 0; u < 16; ++u) acc += expf(xv[u] - head_lds[h + u]) * head_lds[num_q_heads + h + u];
       }
-      for (; h < num_q_heads; ++h)
+      for (; h < h1; ++h)
         acc += expf(x[(int64_t)h * cand_stride + c] - head_lds[h]) * head_lds[num_q_heads + h];
       score[c] = acc;
     }
   }
   __syncthreads();
   if (a.scores_out) {
-    float* so = a.scores_out + (int64_t)j * a.n_out;
+    float* so = a.scores_out + (int64_t)row * a.n_out;
     for (int b = threadIdx.x; b < a.n_out; b += kVoteThreads) {
       const int c = b - a.first;
       so[b] = (c >= 0 && c < n) ? score[c] : -1.0f;
     }
   }
-  int32_t* out = a.sel_idx + (int64_t)j * top_k;
-  if (threadIdx.x == 0) a.sel_cnt[j] = cnt;
+  int32_t* out = a.sel_idx + (int64_t)row * top_k;
+  if (threadIdx.x == 0) a.sel_cnt[row] = cnt;
 
   // f(score bits) for every candidate, in any order. Token mode reads the global score row as
   // float4s (n is a multiple of 64, the row 16-byte aligned) with four loads in flight per thread.
@@ -419,6 +441,22 @@ __global__ __launch_bounds__(kThreads) void token_sum_kernel(const float* __rest
   *reinterpret_cast<float4*>(score + (int64_t)j * cand_stride + c) = acc;
 }
 
+struct LogitsArgs {
+  const float *fingerprints, *k_rep;
+  const ClusterGeo* geo;
+  int parts, n_chunks, cand_stride, sink_blk, num_q_heads, num_kv_heads;
+  float score_scale;
+  float* logits;
+  float2* head_stats;
+};
+
+template <int D, bool kBounds>
+void launch_logits(dim3 grid, const LogitsArgs& a, hipStream_t stream) {
+  block_logits_kernel<D, kBounds><<<grid, kThreads, 0, stream>>>(a.fingerprints, a.k_rep, a.geo, a.parts, a.n_chunks,
+                                                                a.cand_stride, a.sink_blk, a.num_q_heads,
+                                                                a.num_kv_heads, a.score_scale, a.logits, a.head_stats);
+}
+
 }  // namespace
 
 hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
@@ -434,7 +472,7 @@ int selection_chunks(int max_cand) { return (max_cand + kCandChunk - 1) / kCandC
 
 hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
                                int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                               int num_q_heads, int num_kv_heads, int head_dim, float score_scale,
+                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, float score_scale,
                                float* logits, float2* head_stats, hipStream_t stream) {
   if (n_clusters <= 0 || max_cand <= 0) return hipSuccess;
   const int n_chunks = selection_chunks(max_cand);
@@ -442,21 +480,19 @@ hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, co
   const int64_t base = (int64_t)n_clusters * num_kv_heads;
   const int parts = (int)std::min<int64_t>(n_chunks, std::max<int64_t>(1, (kLogitsTargetGroups + base - 1) / base));
   const dim3 grid((unsigned)(base * parts));
+  const LogitsArgs a{fingerprints, k_rep, geo, parts, n_chunks, cand_stride, sink_blk, num_q_heads, num_kv_heads,
+                     score_scale, logits, head_stats};
   if (head_dim == 128)
-    block_logits_kernel<128><<<grid, kThreads, 0, stream>>>(fingerprints, k_rep, geo, parts, n_chunks, cand_stride,
-                                                           sink_blk, num_q_heads, num_kv_heads, score_scale, logits,
-                                                           head_stats);
+    bounds ? launch_logits<128, true>(grid, a, stream) : launch_logits<128, false>(grid, a, stream);
   else
-    block_logits_kernel<64><<<grid, kThreads, 0, stream>>>(fingerprints, k_rep, geo, parts, n_chunks, cand_stride,
-                                                          sink_blk, num_q_heads, num_kv_heads, score_scale, logits,
-                                                          head_stats);
+    bounds ? launch_logits<64, true>(grid, a, stream) : launch_logits<64, false>(grid, a, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo, int n_clusters,
-                            int max_cand, int cand_stride, int sink_blk, int num_q_heads, int top_k, int n_blocks,
-                            float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
-                            hipStream_t stream) {
+                            int max_cand, int cand_stride, int sink_blk, int num_q_heads, int num_kv_heads,
+                            bool per_kv, int top_k, int n_blocks, float* spill, int32_t* sel_idx, int32_t* sel_cnt,
+                            float* scores_out, hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
   VoteArgs a{};
   a.logits = logits;
@@ -464,6 +500,8 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
   a.geo = geo;
   a.n_chunks = selection_chunks(max_cand);
   a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.per_kv = per_kv ? 1 : 0;
   a.top_k = top_k;
   a.cand_stride = cand_stride;
   a.first = sink_blk;
@@ -473,16 +511,16 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
   a.sel_cnt = sel_cnt;
   a.scores_out = scores_out;
   const size_t lds = sizeof(float) * 2 * (size_t)num_q_heads;
-  vote_topk_kernel<false><<<n_clusters, kVoteThreads, lds, stream>>>(a);
+  vote_topk_kernel<false><<<n_clusters * (per_kv ? num_kv_heads : 1), kVoteThreads, lds, stream>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, int n_clusters, int64_t cand_stride,
-                                   int max_cand, int first_token, int num_kv_heads, int top_k, int n_tokens,
-                                   float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
+                                   int max_cand, int first_token, int num_kv_heads, bool per_kv, int top_k,
+                                   int n_tokens, float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
                                    hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
-  if (max_cand > 0) {
+  if (max_cand > 0 && !per_kv) {
     const dim3 grid((unsigned)((max_cand + 4 * kThreads - 1) / (4 * kThreads)), (unsigned)n_clusters);
     token_sum_kernel<<<grid, kThreads, 0, stream>>>(partial, geo, cand_stride, num_kv_heads, spill);
     const hipError_t e = hipGetLastError();
@@ -496,11 +534,12 @@ hipError_t launch_vote_topk_tokens(const float* partial, const ClusterGeo* geo, 
   a.cand_stride = cand_stride;
   a.first = first_token;
   a.n_out = n_tokens;
+  a.per_kv = per_kv ? 1 : 0;
   a.spill = spill;
   a.sel_idx = sel_idx;
   a.sel_cnt = sel_cnt;
   a.scores_out = scores_out;
-  vote_topk_kernel<true><<<n_clusters, kVoteThreads, 0, stream>>>(a);
+  vote_topk_kernel<true><<<n_clusters * (per_kv ? num_kv_heads : 1), kVoteThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 

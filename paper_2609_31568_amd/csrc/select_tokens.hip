@@ -293,23 +293,24 @@ __global__ __launch_bounds__(256) void token_lse_kernel(const float2* __restrict
 }
 
 // grid: (64-row tile of the selection, KV head, cluster). Copies rows [64 u, 64 u + 64) of
-// cluster j's selection for KV head g; rows at or past sel_cnt are written as zeros, tiles past
-// the last partial one are not touched.
+// cluster j's selection (selection row j, or j * Hkv + g with one set per KV head) for KV head g;
+// rows at or past sel_cnt are written as zeros, tiles past the last partial one are not touched.
 template <int D>
 __global__ __launch_bounds__(kGatherThreads) void gather_kernel(const uint16_t* __restrict__ k_pages,
                                                                 const uint16_t* __restrict__ v_pages,
                                                                 const int32_t* __restrict__ block_table,
                                                                 const int32_t* __restrict__ sel_idx,
-                                                                const int32_t* __restrict__ sel_cnt, int top_k,
-                                                                int kpad, int n_tokens, int num_kv_heads,
+                                                                const int32_t* __restrict__ sel_cnt, int per_kv,
+                                                                int top_k, int kpad, int n_tokens, int num_kv_heads,
                                                                 int log2_block, uint16_t* __restrict__ gk,
                                                                 uint16_t* __restrict__ gv) {
   constexpr int kChunksPerRow = D / 8;
   const int u = blockIdx.x, g = blockIdx.y, j = blockIdx.z;
-  int cnt = sel_cnt[j];
+  const int srow = per_kv ? j * num_kv_heads + g : j;
+  int cnt = sel_cnt[srow];
   cnt = cnt < 0 ? 0 : (cnt > top_k ? top_k : cnt);
   if (u * kTokTile >= cnt) return;
-  const int32_t* sel = sel_idx + (int64_t)j * top_k;
+  const int32_t* sel = sel_idx + (int64_t)srow * top_k;
   const int64_t dst0 = (((int64_t)j * num_kv_heads + g) * kpad + u * kTokTile) * D;
   for (int idx = threadIdx.x; idx < kTokTile * kChunksPerRow; idx += kGatherThreads) {
     const int r = idx / kChunksPerRow, c = idx % kChunksPerRow;
@@ -407,18 +408,20 @@ hipError_t launch_token_selection(const float* fingerprints, const uint16_t* k_p
 }
 
 hipError_t launch_gather_selected(const uint16_t* k_pages, const uint16_t* v_pages, const int32_t* block_table,
-                                  const int32_t* sel_idx, const int32_t* sel_cnt, int n_clusters, int top_k,
-                                  int kpad, int n_tokens, int num_kv_heads, int head_dim, int block_size,
+                                  const int32_t* sel_idx, const int32_t* sel_cnt, bool per_kv, int n_clusters,
+                                  int top_k, int kpad, int n_tokens, int num_kv_heads, int head_dim, int block_size,
                                   uint16_t* gk, uint16_t* gv, hipStream_t stream) {
   if (n_clusters <= 0 || top_k <= 0) return hipSuccess;
   const dim3 grid((unsigned)(kpad / kTokTile), (unsigned)num_kv_heads, (unsigned)n_clusters);
   const int lb = block_size == 128 ? 7 : 6;
   if (head_dim == 128)
-    gather_kernel<128><<<grid, kGatherThreads, 0, stream>>>(k_pages, v_pages, block_table, sel_idx, sel_cnt, top_k,
-                                                            kpad, n_tokens, num_kv_heads, lb, gk, gv);
+    gather_kernel<128><<<grid, kGatherThreads, 0, stream>>>(k_pages, v_pages, block_table, sel_idx, sel_cnt,
+                                                            per_kv ? 1 : 0, top_k, kpad, n_tokens, num_kv_heads, lb,
+                                                            gk, gv);
   else
-    gather_kernel<64><<<grid, kGatherThreads, 0, stream>>>(k_pages, v_pages, block_table, sel_idx, sel_cnt, top_k,
-                                                           kpad, n_tokens, num_kv_heads, lb, gk, gv);
+    gather_kernel<64><<<grid, kGatherThreads, 0, stream>>>(k_pages, v_pages, block_table, sel_idx, sel_cnt,
+                                                           per_kv ? 1 : 0, top_k, kpad, n_tokens, num_kv_heads, lb,
+                                                           gk, gv);
   return hipGetLastError();
 }
 

@@ -167,7 +167,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pages,
     const uint16_t* __restrict__ v_pages, const int32_t* __restrict__ block_table,
     const ClusterGeo* __restrict__ geo, const WorkItem* __restrict__ items,
-    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt, int top_k,
+    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt, int per_kv, int top_k,
     int num_q_heads, int num_kv_heads, int n_blocks, float qk_scale_log2, int out_bf16,
     void* __restrict__ out, const uint16_t* __restrict__ gk, const uint16_t* __restrict__ gv, int kpad) {
   using S = AttnShape<D, G, RB>;
@@ -192,7 +192,8 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   const bool row_valid = 32 * rb + row < it.n_rows;
 
   // ---- tile sequence: sink blocks, selected blocks, local window ----
-  int n_sel = sel_cnt[it.cluster];
+  const int srow = per_kv ? it.cluster * num_kv_heads + g : it.cluster;   // selection row
+  int n_sel = sel_cnt[srow];
   n_sel = n_sel < 0 ? 0 : (n_sel > top_k ? top_k : n_sel);
   const int n_sink_tiles = cg.sink_eff * kTilesPerBlock;
   // token-level selection: the selected keys are n_sel gathered rows, the last tile padded
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   const int local0 = cg.lo_blk << LOG2B;
   const int local_end = p0 + it.n_rows;            // keys [local0, local_end) of the window
   const int n_tiles = n_fixed + (local_end - local0 + kKeyTile - 1) / kKeyTile;
-  const int32_t* sel = sel_idx + (int64_t)it.cluster * top_k;
+  const int32_t* sel = sel_idx + (int64_t)srow * top_k;
 
   auto fill_batch = [&](int batch) {
     const int t0 = batch * kDescBatch;
@@ -413,7 +414,7 @@ struct LaunchArgs {
   const WorkItem* items;
   int n_items;
   const int32_t *sel_idx, *sel_cnt;
-  int top_k, num_q_heads, num_kv_heads, n_blocks;
+  int per_kv, top_k, num_q_heads, num_kv_heads, n_blocks;
   float qk_scale_log2;
   int out_bf16;
   void* out;
@@ -427,12 +428,12 @@ hipError_t launch_dgb(const LaunchArgs& a) {
   constexpr int RB = row_blocks(G);
   if (a.gk)
     sparse_attention_kernel<D, G, RB, LOG2B, true><<<a.n_items, G * RB * 64, 0, a.stream>>>(
-        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
-        a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, a.gk, a.gv, a.kpad);
+        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.per_kv, a.top_k,
+        a.num_q_heads, a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, a.gk, a.gv, a.kpad);
   else
     sparse_attention_kernel<D, G, RB, LOG2B, false><<<a.n_items, G * RB * 64, 0, a.stream>>>(
-        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.top_k, a.num_q_heads,
-        a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, nullptr, nullptr, 0);
+        a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.per_kv, a.top_k,
+        a.num_q_heads, a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, nullptr, nullptr, 0);
   return hipGetLastError();
 }
 
@@ -464,14 +465,33 @@ int attention_head_groups(int) { return 1; }   // one work-group covers every qu
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
                                    const WorkItem* items, int n_items, const int32_t* sel_idx,
-                                   const int32_t* sel_cnt, int top_k, int num_q_heads,
+                                   const int32_t* sel_cnt, bool per_kv, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
                                    const uint16_t* gv, int kpad, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
-  const LaunchArgs a{q,           k_pages,      v_pages,  block_table, geo,        items,      n_items,
-                     sel_idx,     sel_cnt,      top_k,    num_q_heads, num_kv_heads, n_blocks, qk_scale_log2,
-                     out_bf16,    out,          gk,       gv,          kpad,       stream};
+  LaunchArgs a{};
+  a.q = q;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.block_table = block_table;
+  a.geo = geo;
+  a.items = items;
+  a.n_items = n_items;
+  a.sel_idx = sel_idx;
+  a.sel_cnt = sel_cnt;
+  a.per_kv = per_kv ? 1 : 0;
+  a.top_k = top_k;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.n_blocks = n_blocks;
+  a.qk_scale_log2 = qk_scale_log2;
+  a.out_bf16 = out_bf16;
+  a.out = out;
+  a.gk = gk;
+  a.gv = gv;
+  a.kpad = kpad;
+  a.stream = stream;
   const int group = num_q_heads / num_kv_heads;
   return head_dim == 128 ? launch_d<128>(group, block_size, a) : launch_d<64>(group, block_size, a);
 }

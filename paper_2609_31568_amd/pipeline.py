@@ -7,16 +7,18 @@ from __future__ import annotations
 
 import numpy as np
 
-from .binding import SCALE_OUT_BF16, Scale, make_config
+from .binding import SCALE_OUT_BF16, SCALE_REP_BOUNDS, Scale, make_config
 
 
 def config_for(*, num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens, local_window,
-               max_tokens, max_clusters, out_bf16=False, softmax_scale=0.0, score_scale=0.0, select_tokens=False):
+               max_tokens, max_clusters, out_bf16=False, softmax_scale=0.0, score_scale=0.0, select_tokens=False,
+               rep_bounds=False, kv_head_sets=False):
     return make_config(num_q_heads=num_q_heads, num_kv_heads=num_kv_heads, head_dim=head_dim,
                        block_size=block_size, sub_chunk=sub_chunk, top_k=top_k, sink_tokens=sink_tokens,
                        local_window=local_window, max_tokens=max_tokens, max_clusters=max_clusters,
                        softmax_scale=softmax_scale, score_scale=score_scale,
-                       out_dtype=SCALE_OUT_BF16 if out_bf16 else 0, select_tokens=select_tokens)
+                       out_dtype=SCALE_OUT_BF16 if out_bf16 else 0, select_tokens=select_tokens,
+                       rep_kind=SCALE_REP_BOUNDS if rep_bounds else 0, kv_head_sets=kv_head_sets)
 
 
 class LayerBuffers:
@@ -26,13 +28,15 @@ class LayerBuffers:
         import torch
 
         nb = n_tokens // cfg.block_size
-        self.k_rep = torch.empty((nb, cfg.num_kv_heads, cfg.head_dim), dtype=torch.float32, device=device)
-        self.sel_idx = torch.empty((n_clusters, max(cfg.top_k, 1)), dtype=torch.int32, device=device)
-        self.sel_cnt = torch.empty((n_clusters,), dtype=torch.int32, device=device)
+        rep = (2, cfg.head_dim) if cfg.rep_kind == SCALE_REP_BOUNDS else (cfg.head_dim,)
+        self.k_rep = torch.empty((nb, cfg.num_kv_heads, *rep), dtype=torch.float32, device=device)
+        rows = n_clusters * (cfg.num_kv_heads if cfg.kv_head_sets else 1)   # selection rows
+        self.sel_idx = torch.empty((rows, max(cfg.top_k, 1)), dtype=torch.int32, device=device)
+        self.sel_cnt = torch.empty((rows,), dtype=torch.int32, device=device)
         odt = torch.bfloat16 if cfg.out_dtype == SCALE_OUT_BF16 else torch.float32
         self.out = torch.empty((n_tokens, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=device)
         n_score = n_tokens if cfg.select_tokens else nb
-        self.scores = torch.empty((n_clusters, n_score), dtype=torch.float32, device=device) if with_scores else None
+        self.scores = torch.empty((rows, n_score), dtype=torch.float32, device=device) if with_scores else None
         self.fingerprints = (torch.empty((n_clusters, cfg.num_q_heads, cfg.head_dim), dtype=torch.float32,
                                          device=device) if with_scores else None)
 

@@ -85,7 +85,7 @@ def check_rounding(gpu: np.ndarray, ref: np.ndarray, what: str):
 U32 = 2.0 ** -24
 
 
-def score_bounds(ref, num_kv_heads: int, score_scale: float = 1.0):
+def score_bounds(ref, num_kv_heads: int, score_scale: float = 1.0, k_bounds=None):
     """First-order error bound of the GPU's fp32 soft-voting scores, per cluster and candidate.
 
     GPU logits are fp32 dot products of the fp32-rounded fingerprint and representative key:
@@ -94,29 +94,38 @@ def score_bounds(ref, num_kv_heads: int, score_scale: float = 1.0):
     dX; the exponent's argument x - max carries a rounding of u |x - max|; exp, the normaliser
     (n_cand terms) and the sum over heads add (n_cand + Hq + 8) u relative. Hence
     |d score_b| <= score_b (2 dX + 2 u R + (n_cand + Hq + 8) u) + 1e-9, with R the logit range.
+    With the channel-wise bounds ``k_bounds`` = (mn, mx), the logit's terms are max(v_i mn_i,
+    v_i mx_i), each within u of its value, so sum_i |v_i k_i| becomes sum_i max(|v_i mn_i|, |v_i mx_i|).
     """
     out = []
     for g, v, sc in zip(ref["geometry"], ref["fingerprints"], ref["scores"]):
         if g.n_cand == 0:
             out.append(np.zeros(0))
             continue
-        kr = ref["k_rep"][g.sink_blk:g.sink_blk + g.n_cand]        # [n, Hkv, d]
         Hq, d = v.shape
         heads_g = (np.arange(Hq) * num_kv_heads) // Hq
-        absdot = np.einsum("hi,nhi->hn", np.abs(v), np.abs(kr[:, heads_g, :])) * abs(score_scale)
+        c = slice(g.sink_blk, g.sink_blk + g.n_cand)
+        if k_bounds is None:
+            kr = ref["k_rep"][c]                                    # [n, Hkv, d]
+            absdot = np.einsum("hi,nhi->hn", np.abs(v), np.abs(kr[:, heads_g, :])) * abs(score_scale)
+            x = np.einsum("hi,nhi->hn", v, kr[:, heads_g, :]) * score_scale
+        else:
+            mn, mx = k_bounds[0][c][:, heads_g, :], k_bounds[1][c][:, heads_g, :]     # [n, Hq, d]
+            absdot = np.maximum(np.abs(v[None] * mn), np.abs(v[None] * mx)).sum(axis=2).T * abs(score_scale)
+            x = np.maximum(v[None] * mn, v[None] * mx).sum(axis=2).T * score_scale
         dX = (d + 2) * U32 * absdot.max()
-        x = np.einsum("hi,nhi->hn", v, kr[:, heads_g, :]) * score_scale
         R = float((x.max(axis=1) - x.min(axis=1)).max())
         rel = 2 * dX + 2 * U32 * R + (g.n_cand + Hq + 8) * U32
         out.append(sc * rel + 1e-9)
     return out
 
 
-def check_scores(gpu_scores: np.ndarray, ref, num_kv_heads: int, what: str):
+def check_scores(gpu_scores: np.ndarray, ref, num_kv_heads: int, what: str, score_scale: float = 1.0, k_bounds=None):
     """Candidates within the bound above; every other entry of the row is -1."""
     worst = 0.0
     nb = gpu_scores.shape[1]
-    for j, (g, sc, bound) in enumerate(zip(ref["geometry"], ref["scores"], score_bounds(ref, num_kv_heads))):
+    bounds = score_bounds(ref, num_kv_heads, score_scale, k_bounds)
+    for j, (g, sc, bound) in enumerate(zip(ref["geometry"], ref["scores"], bounds)):
         row = gpu_scores[j]
         cand = np.arange(g.sink_blk, g.sink_blk + g.n_cand)
         assert np.all(np.delete(row, cand) == -1.0), f"{what} cluster {j}: non-candidate entry is not -1"

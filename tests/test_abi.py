@@ -69,14 +69,17 @@ def _cfg(**over):
     (dict(num_q_heads=72, num_kv_heads=8), -2),   # group of 9 query heads
     (dict(select_tokens=2), -1),
     (dict(select_tokens=1, top_k=1 << 20, max_clusters=4096), -2),   # gathered rows past int32
+    (dict(rep_kind=2), -1),
+    (dict(kv_head_sets=2), -1),
+    (dict(select_tokens=1, rep_kind=1), -2),          # token selection scores the keys themselves
 ])
 def test_init_rejects_bad_config_before_any_hip_call(over, status):
     pk = _pk()
     over = dict(over)
-    raw_tokens = over.pop("select_tokens", None)
+    raw = {k: over.pop(k) for k in ("select_tokens", "rep_kind", "kv_head_sets") if k in over}
     cfg = _cfg(**over)
-    if raw_tokens is not None:
-        cfg.select_tokens = raw_tokens      # the raw field, past make_config's bool conversion
+    for k, v in raw.items():
+        setattr(cfg, k, v)                  # the raw field, past make_config's conversions
     h = ctypes.c_void_p(1234)
     st = pk.lib.scale_init(ctypes.byref(cfg), None, ctypes.byref(h))
     assert st == status
