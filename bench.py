@@ -250,6 +250,13 @@ def time_path(args, w, c, layers, dev, theta=None):
     t1 = time.perf_counter()
     stages = h.stage_times(reset=True)
     calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
+    # per-launch spread: the same steps again, one at a time, outside the timed region
+    per_step = []
+    for _ in range(args.steps):
+        step()
+        st = h.stage_times(reset=True)
+        per_step.append(st["attention"][0] / max(st["attention"][1], 1))
+    per_step.sort()
     overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap and not tokens and not args.kv_sets else None
     h.close()
     del bufs
@@ -327,6 +334,8 @@ def time_path(args, w, c, layers, dev, theta=None):
                         and c == gen.WORKLOADS[w.name].cluster else None),
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
+            "median_launch_ms": round(per_step[len(per_step) // 2], 4),
+            "min_launch_ms": round(per_step[0], 4),
         },
         "mfma_util_pct": round(100 * achieved / PEAK_BF16_TFLOPS, 2),
         "layer_tokens_per_s": round(w.n_tokens * w.layers / (ms_per_step / 1e3), 1),

@@ -72,8 +72,11 @@ constexpr int kMaxClusterSpan = 64;   // largest band width (cluster cap - 1) th
 // Layout plan of the token scoring kernels for one call: fingerprint rows are (cluster, head of the
 // group) with the group padded to gp = a power of two; r_pad rows per KV head in groups of 128;
 // candidates in chunks of chunk_tokens (= tiles_per_chunk 64-token tiles), n_chunks of them.
-constexpr int kMaxTokenChunks = 256;
 constexpr int kTokenTile = 64;        // rows per gathered tile of selected tokens
+constexpr int kTokenChunkTiles = 16;  // candidate tiles per statistics chunk (1024 tokens)
+inline int token_chunks(int max_tokens) {
+  return (max_tokens + kTokenTile * kTokenChunkTiles - 1) / (kTokenTile * kTokenChunkTiles);
+}
 struct TokenPlan {
   int gp, r_pad, n_rowgroups, tiles_per_chunk, n_chunks, chunk_tokens;
 };

@@ -300,7 +300,7 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
     h->kpad = (c.top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
     const int64_t gathered = mc * c.num_kv_heads * h->kpad * c.head_dim;
     ok = dev((void**)&h->d_tok_F, sizeof(uint16_t) * rows * 2 * c.head_dim) &&
-         dev((void**)&h->d_tok_stats, sizeof(float2) * rows * scale::kMaxTokenChunks) &&
+         dev((void**)&h->d_tok_stats, sizeof(float2) * rows * scale::token_chunks(c.max_tokens)) &&
          dev((void**)&h->d_tok_lse, sizeof(float) * rows) &&
          dev((void**)&h->d_tok_partial, sizeof(float) * mc * c.num_kv_heads * (int64_t)c.max_tokens) &&
          dev((void**)&h->d_tok_score, sizeof(float) * mc * (int64_t)c.max_tokens) &&

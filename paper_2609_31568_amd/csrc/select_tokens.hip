@@ -39,7 +39,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kTokTile = kTokenTile;  // candidate tokens per step
 constexpr int kTokThreads = 256;      // 4 waves, one 32-row block each
 constexpr int kRowsPerGroup = 128;
-constexpr int kTargetGroups = 2048;
 constexpr int kGatherThreads = 256;
 constexpr float kStatsHeadroom = 20.f;   // base-2 units a logit may exceed the stats reference by
 
@@ -351,17 +350,16 @@ int token_row_pad(int n_clusters, int group) {
 
 int token_group_pad(int group) { return group <= 1 ? 1 : group <= 2 ? 2 : group <= 4 ? 4 : 8; }
 
-TokenPlan plan_token_selection(int n_clusters, int group, int num_kv_heads, int max_cand) {
+TokenPlan plan_token_selection(int n_clusters, int group, int, int max_cand) {
   TokenPlan p{};
   p.gp = token_group_pad(group);
   p.r_pad = token_row_pad(n_clusters, group);
   p.n_rowgroups = p.r_pad / kRowsPerGroup;
+  // A fixed chunk: a cluster's statistics (and so its scores, bit for bit) do not depend on the
+  // other clusters of the call, which keeps incremental calls equal to one-shot ones.
   const int n_tiles = (max_cand + kTokTile - 1) / kTokTile;
-  const int64_t base = (int64_t)num_kv_heads * p.n_rowgroups;
-  const int chunks_target = (int)std::max<int64_t>(1, (kTargetGroups + base - 1) / base);
-  int tpc = std::max((n_tiles + kMaxTokenChunks - 1) / kMaxTokenChunks, (n_tiles + chunks_target - 1) / chunks_target);
-  p.tiles_per_chunk = std::max(1, tpc);
-  p.n_chunks = n_tiles == 0 ? 0 : (n_tiles + p.tiles_per_chunk - 1) / p.tiles_per_chunk;
+  p.tiles_per_chunk = kTokenChunkTiles;
+  p.n_chunks = (n_tiles + p.tiles_per_chunk - 1) / p.tiles_per_chunk;
   p.chunk_tokens = p.tiles_per_chunk * kTokTile;
   return p;
 }

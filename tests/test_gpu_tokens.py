@@ -211,3 +211,50 @@ def test_token_full_size_sampled(dev, name, c, n_sample, seed):
         mx, rel = gu.check_output(res["out"][at:at + len(rows[i])], o_ref, f"{name} cluster {j}")
         at += len(rows[i])
     gu.log(f"[tokens] {name}: sampled attention ok")
+
+
+def test_token_short_last_subchunk(dev):
+    """n_tokens = 2368: nine sub-chunks of 256 and a last one of 64; clusters of 4; a budget off the
+    tile."""
+    w = gen.WORKLOADS["tiny"].with_(n_tokens=2368)
+    k = 200
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 4)
+    assert cs[-1] == 10
+    res = _run(w, d, cs, dev, k)
+    ref = _oracle(w, d, cs, k)
+    _check_all("token short tail", w, d, cs, k, res, ref)
+
+
+def test_token_incremental_prefill_equals_one_shot(dev):
+    """The outer-chunk loop with token-level selection: each outer chunk of 16 sub-chunks selects
+    tokens and attends against the cache so far; the result equals the one-shot run bit for bit."""
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = gen.WORKLOADS["llama32k"]
+    k = 2048
+    d = gen.make_layer(w)
+    outer = 16
+    cs_full = gen.cluster_starts(w.n_sub_chunks, 8)        # 8 divides 16: no cluster straddles
+    cfg = gu.config(w, len(cs_full) - 1, top_k=k, select_tokens=True)
+    q, kp, vp, bt = (gu.to_dev(d[x], dev) for x in ("q", "k_pages", "v_pages", "block_table"))
+    with pk.Scale(cfg) as h:
+        one = pk.LayerBuffers(cfg, w.n_tokens, len(cs_full) - 1, device=dev)
+        pk.run_layer(h, q, kp, vp, bt, w.n_tokens, cs_full, one)
+        inc = pk.LayerBuffers(cfg, w.n_tokens, len(cs_full) - 1, device=dev)
+        inc.out.fill_(float("nan"))
+        sel_rows = []
+        for o in range(w.n_sub_chunks // outer):
+            n = (o + 1) * outer * w.sub_chunk
+            cs = cs_full[(cs_full >= o * outer) & (cs_full <= (o + 1) * outer)]
+            m = len(cs) - 1
+            h.select_cluster_tokens(q, n, kp, bt, cs, inc.sel_idx[:m], inc.sel_cnt[:m])
+            h.sparse_prefill(q, kp, vp, bt, n, cs, inc.sel_idx[:m], inc.sel_cnt[:m], inc.out)
+            torch.cuda.synchronize()
+            sel_rows.append(inc.sel_idx[:m].clone())
+        torch.cuda.synchronize()
+    assert torch.equal(torch.cat(sel_rows), one.sel_idx)
+    assert torch.equal(one.out, inc.out)
+    gu.log(f"[tokens] incremental = one-shot over {w.n_sub_chunks // outer} outer chunks")

@@ -181,3 +181,22 @@ def test_per_kv_head_sets_full_size_sampled(dev):
         gu.check_output(res["out"][at:at + len(rows[i])], o_ref, f"llama128k cluster {j}")
         at += len(rows[i])
     gu.log(f"[variants] llama128k per-KV-head: {n_exact} of {len(clusters) * Hkv} sampled sets exact")
+
+
+def test_variants_short_last_subchunk(dev):
+    """A short last sub-chunk (2368 tokens: nine of 256 and one of 64) with bound representative
+    keys and per-KV-head sets together, on a two-KV-head shape."""
+    w = gen.Workload("tail2", 1, 8, 2, 64, 2368, 64, 256, 4, 4, 64, 256, 8, 1, 4, 35)
+    Hkv, G = w.num_kv_heads, w.num_q_heads // w.num_kv_heads
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 3)
+    J = len(cs) - 1
+    res = gu.run_gpu(w, d, cs, dev, kv_head_sets=True, rep_bounds=True)
+    ref = _oracle(w, d, cs, kv_head_sets=True, rep_kind="minmax")
+    for g in range(Hkv):
+        view = _group_view(ref, g, Hkv, G, ref["k_rep"])
+        kb = (ref["bounds"][0][:, g:g + 1], ref["bounds"][1][:, g:g + 1])
+        gu.check_scores(res["scores"][g::Hkv], view, 1, f"tail KV head {g}", k_bounds=kb)
+        gu.check_selection(res["sel_idx"][g::Hkv], res["sel_cnt"][g::Hkv], view, EPS_VALID)
+    own = _oracle(w, d, cs, kv_head_sets=True, rep_kind="minmax", external_sel=_gpu_sets(res, J, Hkv))
+    gu.check_output(res["out"], own["output"], "variants short tail")
