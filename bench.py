@@ -396,8 +396,8 @@ def _cluster_stats(cs, theta, l_max, outer, w):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the kernel on one "
-              f"GPU's share is what this build measures)", file=sys.stderr)
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (it measures the path "
+              f"on one GPU's share of the work)", file=sys.stderr)
         sys.exit(2)
     rank = int(os.environ.get("RANK", "0"))
 

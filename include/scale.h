@@ -71,7 +71,7 @@ typedef struct scale_ctx* scale_handle;
 typedef enum {
   SCALE_OK = 0,
   SCALE_ERR_INVALID_ARG = -1,   /* null pointer, inconsistent sizes, malformed cluster_start */
-  SCALE_ERR_UNSUPPORTED = -2,   /* valid but outside what this build supports (head_dim, B, ...) */
+  SCALE_ERR_UNSUPPORTED = -2,   /* valid but outside what this library supports (head_dim, B, ...) */
   SCALE_ERR_OUT_OF_MEMORY = -3, /* scratch allocation failed in scale_init */
   SCALE_ERR_CAPACITY = -4,      /* n_tokens or n_clusters above the capacity given to scale_init */
   SCALE_ERR_HIP = -5            /* a HIP runtime call failed (no device, launch failure, ...) */
