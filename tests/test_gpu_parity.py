@@ -283,3 +283,26 @@ def test_abi_errors_on_device(dev):
         assert lib.scale_retrieval_calls(h.handle, ctypes.byref(n)) == 0 and n.value == 0
         torch.cuda.synchronize()
         assert int(buf.abs().sum()) == 0
+
+
+@pytest.mark.parametrize("name,w,cs", [
+    # one block and one short sub-chunk: no candidates, no sinks, dense causal attention
+    ("one_block", gen.WORKLOADS["tiny"].with_(n_tokens=64), [0, 1]),
+    # a context shorter than one sub-chunk
+    ("short_ctx", gen.WORKLOADS["tiny"].with_(n_tokens=192), [0, 1]),
+    # no budget: sinks and the local window only
+    ("k0", gen.WORKLOADS["tiny"].with_(top_k=0), gen.cluster_starts(8, 2)),
+    # no sink tokens and a zero base window: the window is the cluster itself
+    ("s0_w0", gen.WORKLOADS["tiny"].with_(sink_tokens=0, local_window=0), gen.cluster_starts(8, 4)),
+    # one cluster of every sub-chunk
+    ("one_cluster", gen.WORKLOADS["tiny"], [0, 8]),
+])
+def test_degenerate_shapes(dev, name, w, cs):
+    gu.log(f"[parity] degenerate {name}")
+    d = gen.make_layer(w)
+    cs = np.asarray(cs, dtype=np.int32)
+    res = gu.run_gpu(w, d, cs, dev)
+    ref = _oracle(w, d, cs)
+    gu.check_selection(res["sel_idx"][:, :w.top_k], res["sel_cnt"], ref, EPS_VALID)   # rows hold top_k entries
+    gu.check_output(res["out"], ref["output"], f"degenerate {name}")
+    assert res["calls"] == len(cs) - 1
