@@ -7,8 +7,12 @@
 //                for the query heads h of KV head g (bound form: sigma * sum_i max(v_i mn_i,
 //                v_i mx_i) over the block's channel-wise key bounds), plus each chunk's softmax
 //                partials (max_c x[h][c], sum_c exp(x[h][c] - max)) per head
-//  vote_topk     cluster -> per-head softmax normaliser from the chunk partials, score = sum over
-//                heads of the softmax weights, top-k by (score desc, block index asc), ascending
+//  vote_topk     cluster (or (cluster, KV head) with one set per KV head) -> per-head softmax
+//                normaliser from the chunk partials, score = sum over the voting heads of the
+//                softmax weights, top-k by (score desc, index asc), ascending; token mode takes
+//                the scores of the token scoring kernels (select_tokens.hip)
+//  token_sum     (candidate slice, cluster) -> token scores: the per-KV-head partial scores summed
+//                in KV-head order
 //
 // All of it is HBM/L2-bandwidth work (a few FLOP per byte); every reduction has a fixed order,
 // so two runs give identical bits.
