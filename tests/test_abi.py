@@ -197,3 +197,24 @@ def test_geometry_capacity():
     assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg), 2048, cs.ctypes.data, 8, geo.ctypes.data) == -4
     cs = gen.cluster_starts(16, 8)
     assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg), 4096, cs.ctypes.data, 2, geo.ctypes.data) == -4
+
+
+def test_c_client_of_the_header(tmp_path):
+    """include/scale.h is plain C: a C99 program (tests/c/abi_host.c) compiles against it with
+    warnings as errors, links against libscale.so and runs the host-only calls."""
+    import shutil
+    import subprocess
+
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc is not available")
+    pk = _pk()
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    lib = pk.build.LIB_PATH
+    exe = tmp_path / "abi_host"
+    cmd = ["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(root, "include"),
+           os.path.join(root, "tests", "c", "abi_host.c"), lib, f"-Wl,-rpath,{os.path.dirname(lib)}",
+           "-o", str(exe)]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert run.stdout.count("ok ") == 4
