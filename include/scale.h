@@ -68,7 +68,13 @@ extern "C" {
 
 typedef struct scale_ctx* scale_handle;
 
-typedef enum {
+/* In C++ the status enum has the fixed underlying type int (the size a C enum has), so any code a
+ * C caller passes, known or not, is a valid value on the library's side. */
+typedef enum
+#ifdef __cplusplus
+    : int
+#endif
+{
   SCALE_OK = 0,
   SCALE_ERR_INVALID_ARG = -1,   /* null pointer, inconsistent sizes, malformed cluster_start */
   SCALE_ERR_UNSUPPORTED = -2,   /* valid but outside what this library supports (head_dim, B, ...) */
