@@ -65,25 +65,45 @@ def parse_args():
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_traffic_llama128k.md")
+COUNTER_PROFILE = os.path.join(ROOT, "profiles", "attention_counters_llama128k.md")
 
 
-def measured_traffic(workload_name):
-    """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
-    scaled by the copy-probe factors, or None when the counters were taken on other kernel source
-    or another workload."""
+def profile_block(path):
+    """The JSON block of a committed rocprofv3 summary (taken on the default 128K layer), or None
+    when the file is missing or the counters were taken on other kernel source."""
     import hashlib
     import re
 
-    if workload_name != "llama128k" or not os.path.exists(TRAFFIC_PROFILE):
+    if not os.path.exists(path):
         return None
-    m = re.search(r"```json\n(.*?)\n```", open(TRAFFIC_PROFILE).read(), re.S)
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
     if not m:
         return None
     block = json.loads(m.group(1))
     src = os.path.join(ROOT, block["kernel_source"])
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != block["kernel_source_sha256"]:
         return None
-    return int(block["traffic_bytes"])
+    return block
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the FETCH_SIZE / WRITE_SIZE summary, scaled by the
+    copy-probe factors."""
+    block = profile_block(TRAFFIC_PROFILE)
+    return int(block["traffic_bytes"]) if block else None
+
+
+def counted_mfma(alg_flops, launch_ms):
+    """Executed MFMA work per attention launch from the SQ counter summary: FLOPs from
+    SQ_INSTS_MFMA (masked and padded products included), their ratio to the algorithmic FLOPs,
+    and their rate over the live launch time against the bf16 peak."""
+    block = profile_block(COUNTER_PROFILE)
+    if not block or launch_ms <= 0:
+        return None
+    flops = float(block["mfma_flops_per_dispatch"])
+    return {"flops": flops, "per_algorithmic": round(flops / alg_flops, 4),
+            "frac": round(flops / (launch_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "mfma_busy": block["mfma_busy_fraction"], "clock_ghz": block["clock_ghz"]}
 
 
 def geometry_work(w, geo, tokens=False, bounds=False):
@@ -266,6 +286,9 @@ def time_path(args, w, c, layers, dev, theta=None):
     per_launch = {k: (ms / n if n else 0.0) for k, (ms, n) in stages.items()}
     att_ms = per_launch["attention"]
     achieved = work["attention_flops"] / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
+    # the committed counter summaries describe the default attention launch of the 128K layer only
+    profiled = (w.name == "llama128k" and theta is None and not tokens and not args.kv_sets and not args.rep_bounds
+                and not args.score_scale and not args.out_bf16 and c == gen.WORKLOADS[w.name].cluster)
 
     def gbs(nbytes, ms):
         return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
@@ -330,14 +353,14 @@ def time_path(args, w, c, layers, dev, theta=None):
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": (measured_traffic(w.name) if theta is None and not tokens and not args.kv_sets
-                        and c == gen.WORKLOADS[w.name].cluster else None),
+            "traffic": measured_traffic() if profiled else None,
             "flops_per_launch": work["attention_flops"],
             "avg_launch_ms": round(att_ms, 4),
             "median_launch_ms": round(per_step[len(per_step) // 2], 4),
             "min_launch_ms": round(per_step[0], 4),
         },
         "mfma_util_pct": round(100 * achieved / PEAK_BF16_TFLOPS, 2),
+        "mfma_counted": counted_mfma(work["attention_flops"], att_ms) if profiled else None,
         "layer_tokens_per_s": round(w.n_tokens * w.layers / (ms_per_step / 1e3), 1),
         "stage_ms_per_layer": {k: round(v, 4) for k, v in per_launch.items()},
         "hbm": hbm,

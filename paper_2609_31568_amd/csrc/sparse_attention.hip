@@ -39,11 +39,13 @@
 // LDS layouts:
 //   K   [row][d], row stride d + 8 elements; row 32 b + 8 i + 4 h + j holds key 32 b + 16 h + 4 i + j
 //       (operand reads conflict-free)
-//   V^T [d][key], row stride 68 dwords; the 32 key-pair dwords of row d start at dword
-//       8 ((d / 16) % 4). With 64 banks of 4 bytes, 16-byte reads served 16 lanes at a time and
-//       32-bit writes 32 lanes at a time, both the transposing tile writes and the operand reads
-//       are conflict-free: a 16-row read pass shares one rotation, and the 8 d-chunks of a write
-//       pass land on distinct 4-bank groups.
+//   V^T [d][key], row stride 80 dwords; the 32 key-pair dwords of row d start at dword
+//       4 ((d / 8) % 8). gfx950 serves a ds_read_b128 in 16-lane passes over 64 banks of 4 bytes,
+//       a pass being the four lane quads of one half-wave whose quad index has the same bit
+//       parity, and a ds_write_b32 in 32-lane passes over 32 banks (both measured with bank
+//       conflict counters). Under that model the stride and rotation make both the operand reads
+//       (rows 4q..4q+3 of a pass land on distinct 4-bank groups) and the transposing tile writes
+//       (the 8 d-chunks of a pass on distinct bank groups mod 32) conflict-free.
 // (ds_read_b64_tr_b16 would avoid the transposing writes, but it sustains well under half the
 // bytes per clock of ds_read_b128, and the V operand reads dominate the LDS traffic.)
 #include <math.h>
@@ -88,7 +90,7 @@ struct AttnShape {
   static constexpr int kWaves = G * RB;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKStride = D + 8;                   // elements
-  static constexpr int kVtStrideDw = 68;                   // dwords per V^T row
+  static constexpr int kVtStrideDw = 80;                   // dwords per V^T row
   static constexpr int kKElems = kKeyTile * kKStride;
   static constexpr int kVElems = D * kVtStrideDw * 2;
   static constexpr int kBufElems = kKElems + kVElems;
@@ -156,7 +158,7 @@ __device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u
       int kp, c;
       v_unit<D>(u, kp, c);
       const u32x4 a = vreg[2 * i], b = vreg[2 * i + 1];   // keys 2kp and 2kp+1, d = 8c .. 8c+7
-      uint32_t* dst = vt + (8 * c) * S::kVtStrideDw + 8 * ((c >> 1) & 3) + kp;
+      uint32_t* dst = vt + (8 * c) * S::kVtStrideDw + 4 * (c & 7) + kp;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         dst[(2 * e) * S::kVtStrideDw] = (a[e] & 0xFFFFu) | (b[e] << 16);
@@ -270,13 +272,13 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
 
   // Per-lane LDS element offsets of the operand reads (immediate offsets add the rest).
   const int k_off = row * S::kKStride + 8 * half;
-  // V^T row 32 db + row starts its keys at dword 8 ((32 db + row) / 16 % 4); lane half h reads keys
+  // V^T row 32 db + row starts its keys at dword 4 ((32 db + row) / 8 % 8); lane half h reads keys
   // 16h + [0, 16) of each 32-key block, the 16-byte chunk of keys 32 kb + 16 h + 8 u at dword
   // offset 16 kb + 8 h + 4 u.
   int vt_off[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
-    vt_off[db] = 2 * ((32 * db + row) * S::kVtStrideDw + 8 * ((2 * db + row / 16) & 3) + 8 * half);
+    vt_off[db] = 2 * ((32 * db + row) * S::kVtStrideDw + 4 * ((4 * db + row / 8) & 7) + 8 * half);
 
   fill_batch(0);
   __syncthreads();
