@@ -42,6 +42,11 @@ SHAPES = {
     "g7": (gen.Workload("g7", 1, 14, 2, 128, 4096, 64, 256, 4, 6, 64, 512, 8, 1, 3, 32), 4, 333),
     "g1": (gen.Workload("g1", 1, 2, 2, 64, 4096, 128, 512, 2, 3, 0, 700, 6, 1, 3, 33), 2, 200),
     "g8": (gen.Workload("g8", 1, 8, 1, 64, 2048, 64, 128, 5, 4, 130, 100, 6, 1, 5, 34), 5, 130),
+    # group sizes 2, 3, 5, 6 (fingerprint rows padded to 2, 4, 8, 8 per cluster)
+    "g2": (gen.Workload("g2", 1, 4, 2, 128, 4096, 128, 512, 2, 4, 128, 600, 8, 1, 3, 36), 2, 250),
+    "g3": (gen.Workload("g3", 1, 6, 2, 128, 4096, 64, 256, 3, 6, 64, 512, 8, 1, 3, 37), 3, 190),
+    "g5": (gen.Workload("g5", 1, 5, 1, 128, 4096, 128, 512, 2, 3, 128, 900, 6, 1, 3, 38), 2, 77),
+    "g6": (gen.Workload("g6", 1, 12, 2, 64, 3072, 128, 256, 4, 5, 128, 512, 8, 1, 3, 39), 4, 129),
 }
 
 
