@@ -34,7 +34,7 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def parse_args():
+def parse_args(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -61,7 +61,7 @@ def parse_args():
     ap.add_argument("--out-bf16", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy 1 GiB device to device (reference for HBM byte counters) and exit")
-    return ap.parse_args()
+    return ap.parse_args(argv)
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_traffic_llama128k.md")
@@ -104,6 +104,16 @@ def counted_mfma(alg_flops, launch_ms):
     return {"flops": flops, "per_algorithmic": round(flops / alg_flops, 4),
             "frac": round(flops / (launch_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "mfma_busy": block["mfma_busy_fraction"], "clock_ghz": block["clock_ghz"]}
+
+
+def counters_apply(args, w, c, theta, tokens):
+    """The committed counter summaries describe the default attention launch of the 128K layer
+    only: block-level selection with fixed clusters of the workload's size, mean representative
+    keys, one set per cluster, σ = 1 and fp32 output."""
+    import gen
+
+    return (w.name == "llama128k" and theta is None and not tokens and not args.kv_sets and not args.rep_bounds
+            and not args.score_scale and not args.out_bf16 and c == gen.WORKLOADS[w.name].cluster)
 
 
 def geometry_work(w, geo, tokens=False, bounds=False):
@@ -286,9 +296,7 @@ def time_path(args, w, c, layers, dev, theta=None):
     per_launch = {k: (ms / n if n else 0.0) for k, (ms, n) in stages.items()}
     att_ms = per_launch["attention"]
     achieved = work["attention_flops"] / (att_ms * 1e-3) / 1e12 if att_ms > 0 else 0.0
-    # the committed counter summaries describe the default attention launch of the 128K layer only
-    profiled = (w.name == "llama128k" and theta is None and not tokens and not args.kv_sets and not args.rep_bounds
-                and not args.score_scale and not args.out_bf16 and c == gen.WORKLOADS[w.name].cluster)
+    profiled = counters_apply(args, w, c, theta, tokens)
 
     def gbs(nbytes, ms):
         return round(nbytes / (ms * 1e-3) / 1e9, 1) if ms > 0 else None

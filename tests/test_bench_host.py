@@ -48,10 +48,27 @@ def test_headline_attention_flops():
     assert abs(work["attention_flops"] / 1e12 - 13.178) < 1e-3
 
 
-def test_traffic_block_parses():
-    t = bench.measured_traffic("llama128k")
+def test_counter_blocks_parse():
+    t = bench.measured_traffic()
     assert t is None or t > 3.5 * 2**30       # at least the minimum Q + K + V + O bytes
-    assert bench.measured_traffic("tiny") is None
+    alg = 13178033405952.0
+    m = bench.counted_mfma(alg, 12.5)
+    if m is not None:
+        assert 1.0 <= m["per_algorithmic"] < 1.05          # executed MFMA work covers the visible pairs
+        assert abs(m["frac"] - m["flops"] / 12.5e-3 / 2.5e15) < 1e-3
+    assert bench.counted_mfma(alg, 0.0) is None
+
+
+def test_counters_apply_to_the_default_launch_only():
+    args = bench.parse_args([])
+    w = gen.WORKLOADS["llama128k"]
+    assert bench.counters_apply(args, w, w.cluster, None, False)
+    assert not bench.counters_apply(args, w, 1, None, False)                  # another cluster size
+    assert not bench.counters_apply(args, w, w.cluster, 0.95, False)          # threshold clustering
+    assert not bench.counters_apply(args, w, w.cluster, None, True)           # token-level selection
+    assert not bench.counters_apply(args, gen.WORKLOADS["llama32k"], 8, None, False)
+    for flag in (["--kv-sets"], ["--rep-bounds"], ["--out-bf16"], ["--score-scale", "0.088"]):
+        assert not bench.counters_apply(bench.parse_args(flag), w, w.cluster, None, False), flag
 
 
 def test_more_than_one_gpu_is_refused():
