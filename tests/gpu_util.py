@@ -3,6 +3,7 @@ and compare with the oracle under the acceptance rules."""
 from __future__ import annotations
 
 import math
+import os
 
 import numpy as np
 
@@ -17,7 +18,13 @@ MARGIN = 1e-3
 
 
 def log(msg: str):
+    """Print a progress line; with SCALE_TEST_LOG set, also append it to that file (pytest captures
+    stdout, so a long test stays visible there while it runs)."""
     print(msg, flush=True)
+    path = os.environ.get("SCALE_TEST_LOG")
+    if path:
+        with open(path, "a") as f:
+            f.write(msg + "\n")
 
 
 def to_dev(a: np.ndarray, dev):

@@ -173,9 +173,10 @@ def test_items_with_more_than_256_tiles(dev):
         gu.check_output(res["out"][rows[j]], o_ref, f"wide cluster {j}")
 
 
-@pytest.mark.parametrize("name,seed_rows", [("llama32k", 5), ("llama128k", 6)])
-def test_full_size_llama(dev, name, seed_rows):
-    """Full Llama-3-8B-layer workloads: every selection, and attention on sampled row tiles."""
+@pytest.mark.parametrize("name,seed_rows,every_row", [("llama32k", 5, True), ("llama128k", 6, True)])
+def test_full_size_llama(dev, name, seed_rows, every_row):
+    """Full Llama-3-8B-layer workloads: every selection, and attention on every row of every
+    cluster against the fp64 oracle on the GPU's own selection (2.1 and 13.2 TFLOP of oracle work)."""
     w = gen.WORKLOADS[name]
     gu.log(f"[parity] {name}: generating")
     d = gen.make_layer(w)
@@ -192,15 +193,22 @@ def test_full_size_llama(dev, name, seed_rows):
     gu.log(f"[parity] {name}: {n_exact} of {len(cs) - 1} clusters above the margin, all equal")
     assert res["calls"] == len(cs) - 1
     rng = np.random.default_rng(seed_rows)
-    rows = gu.sample_rows(ref["geometry"], rng)
+    rows = ([np.arange(g.s, g.e) for g in ref["geometry"]] if every_row else gu.sample_rows(ref["geometry"], rng))
     sels = gu.gpu_selections(res, len(cs) - 1)
     worst = (0.0, 0.0)
     for j, g in enumerate(ref["geometry"]):
-        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j], rows[j],
-                                      w.block_size)
+        if every_row:
+            o_ref = oracle.cluster_attention(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j],
+                                             w.block_size)
+        else:
+            o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], g, sels[j],
+                                          rows[j], w.block_size)
         mx, rel = gu.check_output(res["out"][rows[j]], o_ref, f"{name} cluster {j}")
         worst = (max(worst[0], mx), max(worst[1], rel))
-    gu.log(f"[parity] {name}: sampled attention worst max-abs {worst[0]:.2e} rel-L2 {worst[1]:.2e}")
+        if every_row:
+            gu.log(f"[parity] {name}: cluster {j} every row, max-abs {mx:.2e} rel-L2 {rel:.2e}")
+    gu.log(f"[parity] {name}: {'every-row' if every_row else 'sampled'} attention worst max-abs {worst[0]:.2e} "
+           f"rel-L2 {worst[1]:.2e}")
 
 
 def _oracle_clusters(w, d, cs, clusters):
