@@ -34,11 +34,18 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
+# Default warm-up: enough steps for about half a second of GPU work. The clocks of a GPU that has
+# just started working settle within a few hundred milliseconds; a timed region that starts
+# earlier measures the ramp.
+WARMUP_S = 0.5
+
+
 def parse_args(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default: at least 3, and at least %.1f s of them)" % WARMUP_S)
     ap.add_argument("--workload", default="llama128k")
     ap.add_argument("--cluster", type=int, default=0, help="cluster size in sub-chunks (0: the workload's)")
     ap.add_argument("--sweep", default="", help="comma-separated cluster sizes; one JSON line each")
@@ -266,9 +273,13 @@ def time_path(args, w, c, layers, dev, theta=None):
             else:
                 pk.run_layer(h, q, kp, vp, bt, w.n_tokens, lcs, bufs)
 
-    for _ in range(args.warmup):
+    n_warm = 0
+    t_warm = time.perf_counter()
+    while (n_warm < args.warmup if args.warmup is not None
+           else n_warm < 3 or time.perf_counter() - t_warm < WARMUP_S):
         step()
-    torch.cuda.synchronize()
+        n_warm += 1
+        torch.cuda.synchronize()
     h.enable_timing(True)
     h.stage_times(reset=True)
     calls0 = h.retrieval_calls()
@@ -334,7 +345,7 @@ def time_path(args, w, c, layers, dev, theta=None):
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": n_warm,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
