@@ -1,6 +1,6 @@
 """GPU parity: the HIP path, called through the C ABI, against the fp64 oracle on the same seeded
-inputs. Small shapes are compared element by element; the full-size workloads on every
-selection and on sampled attention rows."""
+inputs. Small shapes and the full-size Llama layers are compared on every selection and every
+attention row; the larger workloads on sampled clusters and rows."""
 import numpy as np
 import pytest
 
