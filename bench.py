@@ -64,7 +64,9 @@ def parse_args(argv=None):
     ap.add_argument("--kv-sets", action="store_true", help="one selected set per (cluster, KV head)")
     ap.add_argument("--score-scale", type=float, default=0.0, help="selection logit scale sigma (0: 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tiles", type=int, default=48, help="32-row tiles the oracle attends in its sample")
+    ap.add_argument("--cpu-tiles", type=int, default=48, help="least 32-row tiles the oracle attends in its sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="the oracle's attention sample grows by tiles until it has run this long")
     ap.add_argument("--out-bf16", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy 1 GiB device to device (reference for HBM byte counters) and exit")
@@ -165,14 +167,15 @@ def geometry_work(w, geo, tokens=False, bounds=False):
     }
 
 
-def cpu_baseline(w, data, cs, geo, n_tiles, n_sel_clusters=32, seed=0):
+def cpu_baseline(w, data, cs, geo, min_tiles, min_seconds, n_sel_clusters=32, seed=0):
     """The fp64 oracle as it stands, timed on a bounded sample of one layer and scaled to the
     workload: representative keys of the blocks the sampled clusters score (scaled by block
     count), selection for up to `n_sel_clusters` clusters (all of them when there are no more;
     else the first, the last and random ones, scaled by anchor rows + candidates, the two terms
     its cost is linear in), and attention for `n_tiles` random 32-row tiles of the sampled
-    clusters (scaled by visible (row, key) pairs). Every layer has the same geometry, so the
-    layer time is multiplied by the layer count."""
+    clusters (scaled by visible (row, key) pairs): at least `min_tiles` tiles, and more until the
+    attention sample has run `min_seconds`, so the sample is seconds of CPU work on any host. Every
+    layer has the same geometry, so the layer time is multiplied by the layer count."""
     import numpy as np
     import threadpoolctl
 
@@ -206,8 +209,10 @@ def cpu_baseline(w, data, cs, geo, n_tiles, n_sel_clusters=32, seed=0):
     t_sel = (time.perf_counter() - t1) * sum(cost) / max(sum(cost[j] for j in sample), 1)
 
     sampled_pairs = 0
+    n_tiles = 0
     t2 = time.perf_counter()
-    for _ in range(n_tiles):
+    while n_tiles < min_tiles or time.perf_counter() - t2 < min_seconds:
+        n_tiles += 1
         j = sample[int(rng.integers(0, len(sample)))]
         g = G[j]
         p0 = g.s + 32 * int(rng.integers(0, max(1, (g.e - g.s) // 32)))
@@ -489,7 +494,7 @@ def main():
         variant = args.tokens or args.rep_bounds or args.kv_sets or args.score_scale
         if rank == 0 and not args.no_cpu_baseline and not variant:
             print("[bench] timing the oracle on a sample", file=sys.stderr, flush=True)
-            result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles)
+            result["cpu_baseline"] = cpu_baseline(wc, host0, cs, geo, args.cpu_tiles, args.cpu_seconds)
         if rank == 0:
             print(json.dumps(result), flush=True)
 
