@@ -120,10 +120,10 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
                                    float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
                                    const uint16_t* gv, int kpad, hipStream_t stream);
 
-// Query positions per attention work item for a group of `group` query heads per KV head
-// (a multiple of kTilePositions), and the number of head groups one KV head's query heads are
-// split into. WorkItem.kv_head carries the KV head in its low 16 bits and the head group above.
-int attention_tile_positions(int group);
+// Query positions per attention work item for a group of `group` query heads per KV head and a
+// head dim (a multiple of kTilePositions), and the number of head groups one KV head's query heads
+// are split into. WorkItem.kv_head carries the KV head in its low 16 bits and the head group above.
+int attention_tile_positions(int group, int head_dim);
 int attention_head_groups(int group);
 constexpr int kTilePositions = 32;
 

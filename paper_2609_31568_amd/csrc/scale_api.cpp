@@ -528,7 +528,7 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   // share the sink, selected and local K/V blocks, run together.
   const int B = c.block_size;
   const int group = c.num_q_heads / c.num_kv_heads;
-  const int TP = scale::attention_tile_positions(group);
+  const int TP = scale::attention_tile_positions(group, c.head_dim);
   const int HG = scale::attention_head_groups(group);
   int64_t n_items = 0;
   for (int j = 0; j < n_clusters; ++j)

@@ -2,7 +2,8 @@
 // Eq. 10; the cluster attention step of Algorithm 2, causal).
 //
 // Work item = (cluster j, KV head g, tile of up to 32 * RB query positions). The work-group has
-// G * RB waves: one per (query head of the group, 32-position row block). All of them share the
+// G * RB waves: one per (query head of the group, 32-position row block); up to 8 waves at
+// d = 128 and up to 12 at d = 64 (two or three per SIMD, as the registers allow). All of them share the
 // K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds G * RB * 32 query rows. The
 // tile sequence of an item is: the sink blocks, the cluster's selected blocks, then the local
 // window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own positions
@@ -420,8 +421,13 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     }
 }
 
-// Row blocks per query head for a group of G query heads: up to 8 waves per work-group.
-constexpr int row_blocks(int group) { return group >= 8 ? 1 : (8 / group); }
+// Row blocks per query head for a group of G query heads; the work-group has G * RB waves, one
+// work-group per CU (its LDS). At d = 128 a wave needs 224-232 VGPRs, so two waves fit a SIMD and
+// a work-group takes up to 8; at d = 64 it needs about 140, so three fit and a work-group takes up
+// to 12, the third wave per SIMD hiding more of each wave's tile chain.
+constexpr int row_blocks(int group, int d) {
+  return d == 64 ? (group >= 7 ? 1 : group == 5 ? 2 : 12 / group) : (group >= 8 ? 1 : 8 / group);
+}
 
 struct LaunchArgs {
   const uint16_t *q, *k_pages, *v_pages;
@@ -441,7 +447,7 @@ struct LaunchArgs {
 
 template <int D, int G, int LOG2B>
 hipError_t launch_dgb(const LaunchArgs& a) {
-  constexpr int RB = row_blocks(G);
+  constexpr int RB = row_blocks(G, D);
   if (a.gk)
     sparse_attention_kernel<D, G, RB, LOG2B, true><<<a.n_items, G * RB * 64, 0, a.stream>>>(
         a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.per_kv, a.top_k,
@@ -475,7 +481,9 @@ hipError_t launch_d(int group, int block_size, const LaunchArgs& a) {
 
 }  // namespace
 
-int attention_tile_positions(int group) { return 32 * row_blocks(group); }
+int attention_tile_positions(int group, int head_dim) {
+  return 32 * (head_dim == 64 ? row_blocks(group, 64) : row_blocks(group, 128));
+}
 int attention_head_groups(int) { return 1; }   // one work-group covers every query head of a KV head
 
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,

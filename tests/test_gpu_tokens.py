@@ -47,6 +47,9 @@ SHAPES = {
     "g3": (gen.Workload("g3", 1, 6, 2, 128, 4096, 64, 256, 3, 6, 64, 512, 8, 1, 3, 37), 3, 190),
     "g5": (gen.Workload("g5", 1, 5, 1, 128, 4096, 128, 512, 2, 3, 128, 900, 6, 1, 3, 38), 2, 77),
     "g6": (gen.Workload("g6", 1, 12, 2, 64, 3072, 128, 256, 4, 5, 128, 512, 8, 1, 3, 39), 4, 129),
+    "g2d64": (gen.Workload("g2d64", 1, 4, 2, 64, 4096, 64, 256, 3, 5, 64, 700, 8, 1, 3, 40), 3, 160),
+    "g3d64": (gen.Workload("g3d64", 1, 3, 1, 64, 3072, 128, 512, 2, 3, 128, 600, 6, 1, 3, 42), 2, 300),
+    "g5d64": (gen.Workload("g5d64", 1, 10, 2, 64, 4096, 128, 512, 2, 4, 128, 1000, 6, 1, 3, 43), 2, 200),
 }
 
 
