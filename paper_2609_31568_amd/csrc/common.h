@@ -124,7 +124,7 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
 // head dim (a multiple of kTilePositions), and the number of head groups one KV head's query heads
 // are split into. WorkItem.kv_head carries the KV head in its low 16 bits and the head group above.
 int attention_tile_positions(int group, int head_dim);
-int attention_head_groups(int group);
+int attention_head_groups(int group, int head_dim);
 constexpr int kTilePositions = 32;
 
 }  // namespace scale

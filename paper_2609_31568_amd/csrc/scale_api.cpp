@@ -141,7 +141,7 @@ scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_
 
 int64_t max_work_items(const scale_config& c) {
   const int64_t tiles = ((int64_t)c.max_tokens + scale::kTilePositions - 1) / scale::kTilePositions + c.max_clusters;
-  return tiles * c.num_kv_heads * scale::attention_head_groups(c.num_q_heads / c.num_kv_heads);
+  return tiles * c.num_kv_heads * scale::attention_head_groups(c.num_q_heads / c.num_kv_heads, c.head_dim);
 }
 
 hipEvent_t take_event(scale_ctx* h) {
@@ -523,13 +523,13 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   WorkItem* items = reinterpret_cast<WorkItem*>(geo + n_clusters);
 
   // Work list. Clusters in order; inside a cluster, position tiles from the last (most keys) to
-  // the first; each tile once per KV head, KV head fastest. Work-groups are handed to the 8 XCDs
-  // round-robin, so a KV head stays on one XCD (and its L2) while the tiles of one cluster, which
-  // share the sink, selected and local K/V blocks, run together.
+  // the first; each tile once per (head group, KV head), KV head fastest. Work-groups are handed to
+  // the 8 XCDs round-robin, so a KV head stays on the same XCDs (and their L2) while the tiles of
+  // one cluster, which share the sink, selected and local K/V blocks, run together.
   const int B = c.block_size;
   const int group = c.num_q_heads / c.num_kv_heads;
   const int TP = scale::attention_tile_positions(group, c.head_dim);
-  const int HG = scale::attention_head_groups(group);
+  const int HG = scale::attention_head_groups(group, c.head_dim);
   int64_t n_items = 0;
   for (int j = 0; j < n_clusters; ++j)
     n_items += (int64_t)((geo[j].e - geo[j].s + TP - 1) / TP) * c.num_kv_heads * HG;
@@ -541,8 +541,8 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
     for (int t = n_tiles - 1; t >= 0; --t) {
       const int p0 = g.s + t * TP;
       const int nr = std::min(TP, g.e - p0);
-      for (int kv = 0; kv < c.num_kv_heads; ++kv)
-        for (int hg = 0; hg < HG; ++hg) items[k++] = {j, kv | (hg << 16), p0, nr};
+      for (int hg = 0; hg < HG; ++hg)
+        for (int kv = 0; kv < c.num_kv_heads; ++kv) items[k++] = {j, kv | (hg << 16), p0, nr};
     }
   }
 

@@ -1,9 +1,10 @@
 // Gathered block-sparse flash attention for cluster-level sparse prefill (paper Sec. 5.1.3,
 // Eq. 10; the cluster attention step of Algorithm 2, causal).
 //
-// Work item = (cluster j, KV head g, tile of up to 32 * RB query positions). The work-group has
-// G * RB waves: one per (query head of the group, 32-position row block); up to 8 waves at
-// d = 128 and up to 12 at d = 64 (two or three per SIMD, as the registers allow). All of them share the
+// Work item = (cluster j, KV head g, head group, tile of up to 32 * RB query positions). The
+// work-group has GH * RB waves: one per (query head of the head group, 32-position row block); 8
+// waves at d = 128 and 12 at d = 64 (two or three per SIMD, as the registers allow), the G query
+// heads of a KV head split into G / GH head groups so that every SIMD gets the same number. All of them share the
 // K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds G * RB * 32 query rows. The
 // tile sequence of an item is: the sink blocks, the cluster's selected blocks, then the local
 // window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own positions
@@ -88,9 +89,9 @@ __device__ __forceinline__ float half_weights(const f32x16& s, float mc, float c
   return acc0 + acc1;
 }
 
-template <int D, int G, int RB>
+template <int D, int GH, int RB>
 struct AttnShape {
-  static constexpr int kWaves = G * RB;
+  static constexpr int kWaves = GH * RB;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKStride = D + 8;                   // elements
   static constexpr int kVtStrideDw = 80;                   // dwords per V^T row
@@ -171,15 +172,15 @@ __device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u
   }
 }
 
-template <int D, int G, int RB, int LOG2B, bool TOK>
-__global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
+template <int D, int GH, int RB, int LOG2B, bool TOK>
+__global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pages,
     const uint16_t* __restrict__ v_pages, const int32_t* __restrict__ block_table,
     const ClusterGeo* __restrict__ geo, const WorkItem* __restrict__ items,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt, int per_kv, int top_k,
     int num_q_heads, int num_kv_heads, int n_blocks, float qk_scale_log2, int out_bf16,
     void* __restrict__ out, const uint16_t* __restrict__ gk, const uint16_t* __restrict__ gv, int kpad) {
-  using S = AttnShape<D, G, RB>;
+  using S = AttnShape<D, GH, RB>;
   constexpr int B = 1 << LOG2B;
   constexpr int kTilesPerBlock = B / kKeyTile;
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * S::kBufElems];
@@ -193,8 +194,10 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
   const int lane = tid % 64;
   const int half = lane / 32;
   const int row = lane % 32;
-  const int h = g * G + wave % G;
-  const int rb = wave / G;
+  // query head: KV head g's group of num_q_heads / num_kv_heads heads, head group it.kv_head >> 16
+  // of GH of them, then this wave's head in the head group
+  const int h = g * (num_q_heads / num_kv_heads) + (it.kv_head >> 16) * GH + wave % GH;
+  const int rb = wave / GH;
   const int p0 = it.p0;
   const int wave_p0 = p0 + 32 * rb;
   const int p = wave_p0 + row;
@@ -421,13 +424,19 @@ __global__ __launch_bounds__(G * RB * 64) void sparse_attention_kernel(
     }
 }
 
-// Row blocks per query head for a group of G query heads; the work-group has G * RB waves, one
-// work-group per CU (its LDS). At d = 128 a wave needs 224-232 VGPRs, so two waves fit a SIMD and
-// a work-group takes up to 8; at d = 64 it needs about 140, so three fit and a work-group takes up
-// to 12, the third wave per SIMD hiding more of each wave's tile chain.
-constexpr int row_blocks(int group, int d) {
-  return d == 64 ? (group >= 7 ? 1 : group == 5 ? 2 : 12 / group) : (group >= 8 ? 1 : 8 / group);
+// Shape of the work-group: GH query heads (a head group of the G heads of a KV head) times RB row
+// blocks, one wave each, one work-group per CU (its LDS). At d = 128 a wave needs 224-232 VGPRs,
+// so two waves share a SIMD and a work-group has 8; at d = 64 it needs about 140, so three share a
+// SIMD and a work-group has 12. GH is the largest divisor of G that fills the waves exactly (8 at
+// d = 128: GH = 1 for G = 3, 5, 7, GH = 2 for G = 6; 12 at d = 64: GH = 1 for G = 5, 7, GH = 4
+// for G = 8), so every SIMD carries the same number of waves.
+constexpr int waves_per_group(int d) { return d == 64 ? 12 : 8; }
+constexpr int heads_per_group(int group, int d) {
+  for (int gh = group; gh > 1; --gh)
+    if (group % gh == 0 && waves_per_group(d) % gh == 0) return gh;
+  return 1;
 }
+constexpr int row_blocks(int gh, int d) { return waves_per_group(d) / gh; }
 
 struct LaunchArgs {
   const uint16_t *q, *k_pages, *v_pages;
@@ -445,36 +454,34 @@ struct LaunchArgs {
   hipStream_t stream;
 };
 
-template <int D, int G, int LOG2B>
+template <int D, int GH, int LOG2B>
 hipError_t launch_dgb(const LaunchArgs& a) {
-  constexpr int RB = row_blocks(G, D);
+  constexpr int RB = row_blocks(GH, D);
   if (a.gk)
-    sparse_attention_kernel<D, G, RB, LOG2B, true><<<a.n_items, G * RB * 64, 0, a.stream>>>(
+    sparse_attention_kernel<D, GH, RB, LOG2B, true><<<a.n_items, GH * RB * 64, 0, a.stream>>>(
         a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.per_kv, a.top_k,
         a.num_q_heads, a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, a.gk, a.gv, a.kpad);
   else
-    sparse_attention_kernel<D, G, RB, LOG2B, false><<<a.n_items, G * RB * 64, 0, a.stream>>>(
+    sparse_attention_kernel<D, GH, RB, LOG2B, false><<<a.n_items, GH * RB * 64, 0, a.stream>>>(
         a.q, a.k_pages, a.v_pages, a.block_table, a.geo, a.items, a.sel_idx, a.sel_cnt, a.per_kv, a.top_k,
         a.num_q_heads, a.num_kv_heads, a.n_blocks, a.qk_scale_log2, a.out_bf16, a.out, nullptr, nullptr, 0);
   return hipGetLastError();
 }
 
-template <int D, int G>
+template <int D, int GH>
 hipError_t launch_dg(int block_size, const LaunchArgs& a) {
-  return block_size == 128 ? launch_dgb<D, G, 7>(a) : launch_dgb<D, G, 6>(a);
+  return block_size == 128 ? launch_dgb<D, GH, 7>(a) : launch_dgb<D, GH, 6>(a);
 }
 
 template <int D>
 hipError_t launch_d(int group, int block_size, const LaunchArgs& a) {
-  switch (group) {
+  switch (heads_per_group(group, D)) {
     case 1: return launch_dg<D, 1>(block_size, a);
     case 2: return launch_dg<D, 2>(block_size, a);
-    case 3: return launch_dg<D, 3>(block_size, a);
+    case 3: if constexpr (D == 64) return launch_dg<D, 3>(block_size, a); else return hipErrorInvalidValue;
     case 4: return launch_dg<D, 4>(block_size, a);
-    case 5: return launch_dg<D, 5>(block_size, a);
-    case 6: return launch_dg<D, 6>(block_size, a);
-    case 7: return launch_dg<D, 7>(block_size, a);
-    case 8: return launch_dg<D, 8>(block_size, a);
+    case 6: if constexpr (D == 64) return launch_dg<D, 6>(block_size, a); else return hipErrorInvalidValue;
+    case 8: if constexpr (D == 128) return launch_dg<D, 8>(block_size, a); else return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }
@@ -482,9 +489,12 @@ hipError_t launch_d(int group, int block_size, const LaunchArgs& a) {
 }  // namespace
 
 int attention_tile_positions(int group, int head_dim) {
-  return 32 * (head_dim == 64 ? row_blocks(group, 64) : row_blocks(group, 128));
+  return 32 * (head_dim == 64 ? row_blocks(heads_per_group(group, 64), 64)
+                              : row_blocks(heads_per_group(group, 128), 128));
 }
-int attention_head_groups(int) { return 1; }   // one work-group covers every query head of a KV head
+int attention_head_groups(int group, int head_dim) {
+  return group / (head_dim == 64 ? heads_per_group(group, 64) : heads_per_group(group, 128));
+}
 
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
