@@ -36,9 +36,7 @@
 //
 // Pipelining: LDS holds two tile buffers, and two register sets stage the global loads. A tile's
 // loads are issued two tiles ahead; they are written to LDS at the end of the tile before it, and
-// one barrier per tile separates the phases. Work-groups of 320-448 threads at d = 128 (group
-// sizes 3, 5, 6, 7) need up to 8 loads per thread and tile instead of 4; they use one register
-// set and issue each tile's loads one tile ahead, which keeps them clear of register spills.
+// one barrier per tile separates the phases.
 //
 // LDS layouts:
 //   K   [row][d], row stride d + 8 elements; row 32 b + 8 i + 4 h + j holds key 32 b + 16 h + 4 i + j
@@ -290,16 +288,12 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
   __syncthreads();
   if (n_tiles > kDescBatch) fill_batch(1);
   // Tile j's global loads are issued two tiles ahead, in iteration j - 2, into register set j % 2,
-  // and stored into LDS buffer j % 2 at the end of iteration j - 1 (one ahead: issued in iteration
-  // j - 1 into the one set). Loads past the last tile re-read the last tile (never stored), which
-  // keeps the wait counts static.
-  // Work-groups of fewer than 512 threads at d = 128 need more than four 16-byte loads per thread
-  // and tile; they load one tile ahead, from one register set, to stay within the register file.
-  constexpr int kAhead = S::kPer + 2 * S::kVPer > 4 ? 1 : 2;
+  // and stored into LDS buffer j % 2 at the end of iteration j - 1. Loads past the last tile
+  // re-read the last tile (never stored), which keeps the wait counts static.
   if (n_tiles > 0) {
     load_at(0, kreg0, vreg0);
     store_tile<S, D>(kreg0, vreg0, lds, tid);
-    if constexpr (kAhead == 2) load_at(min(1, n_tiles - 1), kreg1, vreg1);
+    load_at(min(1, n_tiles - 1), kreg1, vreg1);
   }
   __syncthreads();
 
@@ -307,7 +301,7 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
                   u32x4 (&vs)[2 * S::kVPer]) {
     const int buf = t & 1;
     if (t > 0 && t % kDescBatch == 0 && t + kDescBatch < n_tiles) fill_batch(t / kDescBatch + 1);
-    load_at(min(t + kAhead, n_tiles - 1), kl, vl);
+    load_at(min(t + 2, n_tiles - 1), kl, vl);
 
     const uint16_t* k_lds = lds + buf * S::kBufElems;
     const uint16_t* v_lds = k_lds + S::kKElems;
@@ -395,13 +389,9 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
     if (t + 1 < n_tiles) store_tile<S, D>(ks, vs, lds + (buf ^ 1) * S::kBufElems, tid);
     __syncthreads();
   };
-  if constexpr (kAhead == 2) {
-    for (int t = 0; t < n_tiles; t += 2) {
-      body(t, kreg0, vreg0, kreg1, vreg1);
-      if (t + 1 < n_tiles) body(t + 1, kreg1, vreg1, kreg0, vreg0);
-    }
-  } else {
-    for (int t = 0; t < n_tiles; ++t) body(t, kreg0, vreg0, kreg0, vreg0);
+  for (int t = 0; t < n_tiles; t += 2) {
+    body(t, kreg0, vreg0, kreg1, vreg1);
+    if (t + 1 < n_tiles) body(t + 1, kreg1, vreg1, kreg0, vreg0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
