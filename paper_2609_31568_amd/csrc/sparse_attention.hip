@@ -5,7 +5,7 @@
 // work-group has GH * RB waves: one per (query head of the head group, 32-position row block); 8
 // waves at d = 128 and 12 at d = 64 (two or three per SIMD, as the registers allow), the G query
 // heads of a KV head split into G / GH head groups so that every SIMD gets the same number. All of them share the
-// K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds G * RB * 32 query rows. The
+// K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds GH * RB * 32 query rows. The
 // tile sequence of an item is: the sink blocks, the cluster's selected blocks, then the local
 // window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own positions
 // need the causal mask. The page of every tile is resolved once per item into an LDS table. The
