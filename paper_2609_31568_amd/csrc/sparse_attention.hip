@@ -4,15 +4,15 @@
 // Work item = (cluster j, KV head g, head group, tile of up to 32 * RB query positions). The
 // work-group has GH * RB waves: one per (query head of the head group, 32-position row block); 8
 // waves at d = 128 and 12 at d = 64 (two or three per SIMD, as the registers allow), the G query
-// heads of a KV head split into G / GH head groups so that every SIMD gets the same number. All of them share the
-// K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds GH * RB * 32 query rows. The
-// tile sequence of an item is: the sink blocks, the cluster's selected blocks, then the local
-// window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own positions
-// need the causal mask. The page of every tile is resolved once per item into an LDS table. The
-// selected set is the cluster's row of sel_idx, or the (cluster, KV head) row with one set per KV
-// head. Token-level selection (TOK) reads the selected keys from the rows gathered per (cluster,
-// KV head); their tiles are marked by negative table entries, and the padding rows of a partial
-// last gathered tile are masked like the causal mask.
+// heads of a KV head split into G / GH head groups so that every SIMD gets the same number. All of
+// them share the K/V tiles staged in LDS, so one 64-key tile fetched from L2 feeds GH * RB * 32
+// query rows. The tile sequence of an item is: the sink blocks, the cluster's selected blocks, then
+// the local window [lo_blk * B, last position] in 64-key tiles; only tiles reaching a wave's own
+// positions need the causal mask. The page of every tile is resolved once per item into an LDS
+// table. The selected set is the cluster's row of sel_idx, or the (cluster, KV head) row with one
+// set per KV head. Token-level selection (TOK) reads the selected keys from the rows gathered per
+// (cluster, KV head); their tiles are marked by negative table entries, and the padding rows of a
+// partial last gathered tile are masked like the causal mask.
 //
 // Per 64-key tile and wave (d = head dim, 32 query rows of one head):
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q held in registers
