@@ -64,7 +64,8 @@ def parse_args(argv=None):
     ap.add_argument("--kv-sets", action="store_true", help="one selected set per (cluster, KV head)")
     ap.add_argument("--score-scale", type=float, default=0.0, help="selection logit scale sigma (0: 1)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tiles", type=int, default=48, help="least 32-row tiles the oracle attends in its sample")
+    ap.add_argument("--cpu-tiles", type=int, default=2,
+                    help="least row chunks (the oracle's own 512-row chunks of a cluster) in its attention sample")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle's attention sample grows by tiles until it has run this long")
     ap.add_argument("--out-bf16", action="store_true")
@@ -167,15 +168,19 @@ def geometry_work(w, geo, tokens=False, bounds=False):
     }
 
 
+ORACLE_CHUNK = 512   # rows per call of the oracle's own full-layer attention (its cluster_attention)
+
+
 def cpu_baseline(w, data, cs, geo, min_tiles, min_seconds, n_sel_clusters=32, seed=0):
     """The fp64 oracle as it stands, timed on a bounded sample of one layer and scaled to the
     workload: representative keys of the blocks the sampled clusters score (scaled by block
     count), selection for up to `n_sel_clusters` clusters (all of them when there are no more;
     else the first, the last and random ones, scaled by anchor rows + candidates, the two terms
-    its cost is linear in), and attention for `n_tiles` random 32-row tiles of the sampled
-    clusters (scaled by visible (row, key) pairs): at least `min_tiles` tiles, and more until the
-    attention sample has run `min_seconds`, so the sample is seconds of CPU work on any host. Every
-    layer has the same geometry, so the layer time is multiplied by the layer count."""
+    its cost is linear in), and attention for random row chunks of the sampled clusters, each one
+    of the oracle's own chunks (up to 512 rows from the cluster start, as its full-layer pass
+    takes them; scaled by visible (row, key) pairs): at least `min_tiles` chunks, and more until
+    the attention sample has run `min_seconds`, so the sample is seconds of CPU work on any host.
+    Every layer has the same geometry, so the layer time is multiplied by the layer count."""
     import numpy as np
     import threadpoolctl
 
@@ -215,8 +220,8 @@ def cpu_baseline(w, data, cs, geo, min_tiles, min_seconds, n_sel_clusters=32, se
         n_tiles += 1
         j = sample[int(rng.integers(0, len(sample)))]
         g = G[j]
-        p0 = g.s + 32 * int(rng.integers(0, max(1, (g.e - g.s) // 32)))
-        rows = np.arange(p0, min(p0 + 32, g.e))
+        p0 = g.s + ORACLE_CHUNK * int(rng.integers(0, max(1, -(-(g.e - g.s) // ORACLE_CHUNK))))
+        rows = np.arange(p0, min(p0 + ORACLE_CHUNK, g.e))
         oracle.attention_rows(data["q"], data["k_pages"], data["v_pages"], data["block_table"], g, sels[j], rows, B)
         sampled_pairs += len(rows) * (g.sink_eff + g.sel_cnt) * B + int(sum(p - g.lo_blk * B + 1 for p in rows))
     t_att_raw = time.perf_counter() - t2
@@ -229,7 +234,7 @@ def cpu_baseline(w, data, cs, geo, min_tiles, min_seconds, n_sel_clusters=32, se
         "cores": cores,
         "kind": "oracle",
         "sample": (f"fp64 numpy oracle on layer 0: representative keys of {n_rep} of {w.n_tokens // B} blocks, "
-                   f"selection of {len(sample)} of {J} clusters, attention of {n_tiles} random 32-row tiles x "
+                   f"selection of {len(sample)} of {J} clusters, attention of {n_tiles} random {ORACLE_CHUNK}-row chunks x "
                    f"{w.num_q_heads} heads ({sampled_pairs} of {total_pairs} visible (row, key) pairs); each part "
                    f"scaled to the layer, x{w.layers} layers"),
         "seconds_measured": round(measured, 2),
