@@ -46,6 +46,9 @@ SMALL = {
     "gqa": gen.Workload("gqa", 1, 8, 2, 32, 1024, 32, 128, 3, 3, 32, 128, 6, 1, 3, 11),
     # group size 7 (Qwen-like), ragged last cluster
     "g7": gen.Workload("g7", 1, 7, 1, 32, 768, 32, 64, 5, 2, 64, 96, 5, 1, 4, 12),
+    # a window (100) and a sink (40) off the block grid (32): with one sub-chunk (64 rows) per
+    # cluster the window starts inside a block and is rounded down (R10), the sink rounds up (R11)
+    "offgrid": gen.Workload("offgrid", 1, 4, 1, 32, 1024, 32, 64, 1, 3, 40, 100, 6, 1, 3, 13),
 }
 
 
@@ -68,7 +71,7 @@ def test_wide_window_is_dense():
     assert np.max(np.abs(r["output"] - ref)) < 1e-12
 
 
-@pytest.mark.parametrize("name,c", [("tiny", 4), ("tiny", 1), ("gqa", 3), ("gqa", 1), ("g7", 5)])
+@pytest.mark.parametrize("name,c", [("tiny", 4), ("tiny", 1), ("gqa", 3), ("gqa", 1), ("g7", 5), ("offgrid", 1)])
 def test_brute_force_selection_and_attention(name, c):
     """Selection = best-total-score k-subset, attention = masked dense softmax (P2 at c=1, P3)."""
     w = SMALL[name].with_(cluster=c)
@@ -287,3 +290,29 @@ def test_topic_matched_blocks_rank_first():
             hits += len(set(matched) & set(int(x) for x in sel))
             total += len(matched)
     assert total > 10 and hits / total >= 0.9
+
+
+@pytest.mark.parametrize("scores,k,sel,margin", [
+    # distinct scores: order 3.0 (13), 2.0 (11), 1.25 (12), 1.0 (14), 0.5 (10); the gap below the
+    # k-th is 2.0 - 1.25 (the gaps next to it, 1.0 and 0.25, would be the off-by-one readings)
+    ([0.5, 2.0, 1.25, 3.0, 1.0], 2, [11, 13], 0.75),
+    ([0.5, 2.0, 1.25, 3.0, 1.0], 1, [13], 1.0),
+    ([0.5, 2.0, 1.25, 3.0, 1.0], 4, [11, 12, 13, 14], 0.5),
+    # one candidate more than k: the gap to the only unselected one
+    ([1.0, 4.0, 2.5], 2, [11, 12], 1.5),
+    # a tie straddling position k: the lower index of the two 2.0s is taken, and the margin is 0
+    ([2.0, 1.0, 2.0, 3.0], 2, [10, 13], 0.0),
+    # a tie inside the top-k does not make the margin 0
+    ([3.0, 3.0, 1.0], 2, [10, 11], 2.0),
+    # no budget, or every candidate selected: nothing is decided, the margin is infinite
+    ([0.5, 2.0, 1.25], 0, [], math.inf),
+    ([0.5, 2.0, 1.25], 3, [10, 11, 12], math.inf),
+    ([0.5, 2.0, 1.25], 7, [10, 11, 12], math.inf),
+])
+def test_topk_margin_closed_form(scores, k, sel, margin):
+    """R12 on hand-picked scores (candidates start at block 10): the selection and the margin
+    score_(k) - score_(k+1) in (score desc, index asc) order, which decides where the GPU's indices
+    must equal the oracle's."""
+    got, m = oracle.select_topk(np.asarray(scores, dtype=np.float64), 10, k)
+    assert got.tolist() == sel
+    assert m == margin
