@@ -13,7 +13,7 @@
  *   scale_sparse_prefill  block-sparse attention of every query row over sink blocks, the
  *                         cluster's selected blocks and the causal local window
  *
- * and, on a handle created with select_tokens = 1, its token-level form (the paper's own
+ * and, on a handle created by scale_init_variant with select_tokens = 1, its token-level form (the paper's own
  * granularity): scale_select_cluster_tokens scores every single candidate token with its own key,
  * top_k counts tokens, and scale_sparse_prefill attends over the selected tokens.
  *
@@ -99,7 +99,7 @@ typedef struct {
   int32_t head_dim;      /* d: 64 or 128                                                     */
   int32_t block_size;    /* B: 64 or 128 tokens per KV block / page                          */
   int32_t sub_chunk;     /* L: query rows per sub-chunk, a positive multiple of B            */
-  int32_t top_k;         /* k >= 0 blocks (tokens if select_tokens) selected per cluster;
+  int32_t top_k;         /* k >= 0 blocks (tokens with select_tokens) selected per cluster;
                             sel_idx rows hold k entries                                      */
   int32_t sink_tokens;   /* S >= 0: attention-sink tokens, rounded up to whole blocks        */
   int32_t local_window;  /* W >= 0: base local window in tokens                              */
@@ -108,23 +108,35 @@ typedef struct {
   float softmax_scale;   /* attention logit scale; 0 means 1/sqrt(head_dim) (Eqs. 1, 10)     */
   float score_scale;     /* selection logit scale sigma; 0 means 1.0 (the literal v . k)     */
   int32_t out_dtype;     /* scale_out_dtype of the attention output                          */
+} scale_config;
+
+/* Variants of the selection step a handle can run instead of the default (all fields 0): the
+ * block-level mean-key selection with one set per cluster. Passed to scale_init_variant only, so
+ * scale_config keeps the fields of the default path. */
+typedef struct {
   int32_t select_tokens; /* 0: block-level selection; 1: token-level selection (top_k counts
-                            tokens; scale_init also allocates the token calls' scratch)      */
+                            tokens; scale_init_variant also allocates the token calls' scratch)  */
   int32_t rep_kind;      /* scale_rep_kind of block-level selection (SCALE_REP_BOUNDS with
-                            select_tokens = 1 is SCALE_ERR_UNSUPPORTED)                      */
+                            select_tokens = 1 is SCALE_ERR_UNSUPPORTED)                        */
   int32_t kv_head_sets;  /* 0: one selected set per cluster, voted by every query head (Sec.
                             5.1.3 head soft-voting); 1: one set per (cluster, KV head), voted by
                             that KV head's query heads only, and query head h attends over the
                             set of its KV head (sel_idx, sel_cnt and scores_out gain a KV-head
                             dimension)                                                         */
-} scale_config;
+} scale_variant;
 
 /* Create a handle bound to the current HIP device and to `hip_stream` (a hipStream_t; NULL is
  * the default stream). Validates `cfg` first (INVALID_ARG / UNSUPPORTED before any HIP call),
  * then allocates the scratch the calls need for cfg->max_tokens and cfg->max_clusters, once.
  * On success *out holds the handle; on failure *out is NULL. Paper: the per-layer inputs of
- * Algorithm 2 (Q, the KV cache, L, the budgets k, n_init and n_local). */
+ * Algorithm 2 (Q, the KV cache, L, the budgets k, n_init and n_local). The handle runs the
+ * default selection (block level, mean representative keys, one set per cluster). */
 scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle* out);
+
+/* scale_init for a selection variant (see scale_variant); variant NULL is the default path, the
+ * same as scale_init. */
+scale_status scale_init_variant(const scale_config* cfg, const scale_variant* variant, void* hip_stream,
+                                scale_handle* out);
 
 /* Release the handle and its scratch (synchronises the handle's stream first). NULL is a no-op. */
 void scale_free(scale_handle h);
@@ -157,17 +169,20 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
  * sel_cnt (device) receives min(k, n_cand) per cluster (also host-computable from the geometry).
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens / B]; candidate entries
  *   receive their score, every other entry -1.
- * fingerprints_out (optional, may be NULL): device fp32 [n_clusters][Hq][d] anchor fingerprints.
- * With rep_kind = SCALE_REP_BOUNDS, k_rep holds the channel-wise bounds and x[h][b] = score_scale *
- * sum_i max(v[h][i] mn[b][g(h)][i], v[h][i] mx[b][g(h)][i]). With kv_head_sets = 1, score and top-k
- * are taken per (cluster j, KV head g) over the query heads of g only, into row j * Hkv + g of
- * sel_idx, sel_cnt and scores_out.
+ * Arithmetic: the fingerprint is an fp64 sum of the bf16 rows; logits, the per-head softmax
+ *   normalisers and the score sum over heads are fp64; each score is rounded once to fp32, and the
+ *   top-k orders those fp32 scores (two candidates whose fp64 scores round to one fp32 value tie,
+ *   and the lower index wins).
+ * On a handle whose variant has rep_kind = SCALE_REP_BOUNDS, k_rep holds the channel-wise bounds
+ * and x[h][b] = score_scale * sum_i max(v[h][i] mn[b][g(h)][i], v[h][i] mx[b][g(h)][i]). With
+ * kv_head_sets = 1, score and top-k are taken per (cluster j, KV head g) over the query heads of g
+ * only, into row j * Hkv + g of sel_idx, sel_cnt and scores_out.
  * Each call adds n_clusters to the handle's retrieval-call counter. On a select_tokens handle
  * this call returns SCALE_ERR_UNSUPPORTED (use scale_select_cluster_tokens). */
 scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens,
                                   const float* k_rep, const int32_t* cluster_start,
                                   int32_t n_clusters, int32_t* sel_idx, int32_t* sel_cnt,
-                                  float* scores_out, float* fingerprints_out);
+                                  float* scores_out);
 
 /* Token-level cluster selection (Eq. 9 with head soft-voting, Sec. 5.1.3, at the granularity of
  * single tokens); handles created with select_tokens = 1 only (else SCALE_ERR_UNSUPPORTED):
@@ -179,7 +194,7 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
  *              in ascending order into sel_idx[j][0..sel_cnt), the rest of the row -1.
  * The logits are computed on the matrix cores from a two-piece bf16 split of the fp32
  * fingerprint (relative representation error <= 2^-18) with fp32 accumulation.
- * cluster_start, sel_cnt and fingerprints_out as for scale_select_cluster.
+ * cluster_start and sel_cnt as for scale_select_cluster.
  * scores_out (optional, may be NULL): device fp32 [n_clusters][n_tokens]; candidate entries
  *   receive their score, every other entry -1.
  * kv_head_sets = 1 works as for scale_select_cluster (rows j * Hkv + g).
@@ -187,8 +202,13 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
 scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens,
                                          const uint16_t* k_pages, const int32_t* block_table,
                                          const int32_t* cluster_start, int32_t n_clusters,
-                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
-                                         float* fingerprints_out);
+                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out);
+
+/* The anchor fingerprints of the most recent selection call on this handle (scale_select_cluster
+ * or scale_select_cluster_tokens), each the fp32 rounding of the exact mean of its anchor rows:
+ * device fp32 [n_clusters][Hq][d], copied on the handle's stream (no synchronisation). n_clusters
+ * may not exceed that call's cluster count (INVALID_ARG, also when no selection call was made). */
+scale_status scale_fingerprints(scale_handle h, float* fingerprints, int32_t n_clusters);
 
 /* Block-sparse prefill attention (Eq. 10): for every row p of every cluster and every query
  * head h, out[p][h] = softmax over Kset(p) of (q[p][h] . k_t * softmax_scale) weighted sum of
@@ -263,10 +283,10 @@ scale_status scale_stage_times(scale_handle h, double* ms, int64_t* launches, in
 
 /* Host-only geometry of each cluster, exactly as the calls above use it (no HIP call; usable
  * without a device). For cluster j, writes geo[j*6 + 0..5] =
- *   { s, e, lo_blk, sink_eff, n_cand, sel_cnt }  (n_cand and sel_cnt in tokens on a
- *   select_tokens config).
- * Same validation of cfg and cluster_start as the calls above. */
-scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens,
+ *   { s, e, lo_blk, sink_eff, n_cand, sel_cnt }  (n_cand and sel_cnt in tokens when variant has
+ *   select_tokens = 1; variant may be NULL).
+ * Same validation of cfg, variant and cluster_start as the calls above. */
+scale_status scale_cluster_geometry(const scale_config* cfg, const scale_variant* variant, int32_t n_tokens,
                                     const int32_t* cluster_start, int32_t n_clusters,
                                     int32_t* geo);
 

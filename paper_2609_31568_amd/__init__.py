@@ -4,5 +4,6 @@ The computation lives in libscale.so (hand-written HIP kernels behind the C ABI 
 include/scale.h); this package is its ctypes binding plus a per-layer driver.
 """
 from .binding import *  # noqa: F401,F403
-from .binding import EXPORTS, STAGES, Scale, ScaleError, make_config, scale_config, status_string  # noqa: F401
+from .binding import (EXPORTS, STAGES, Config, Scale, ScaleError, make_config, scale_config,  # noqa: F401
+                      scale_variant, status_string)
 from .pipeline import LayerBuffers, config_for, run_layer  # noqa: F401

@@ -29,6 +29,7 @@ EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
     "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range", "scale_select_cluster_tokens",
+    "scale_init_variant", "scale_fingerprints",
 )
 STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster", "gather")
 
@@ -54,10 +55,31 @@ class scale_config(ctypes.Structure):
         ("softmax_scale", ctypes.c_float),
         ("score_scale", ctypes.c_float),
         ("out_dtype", ctypes.c_int32),
+    ]
+
+
+class scale_variant(ctypes.Structure):
+    _fields_ = [
         ("select_tokens", ctypes.c_int32),
         ("rep_kind", ctypes.c_int32),
         ("kv_head_sets", ctypes.c_int32),
     ]
+
+
+class Config:
+    """A scale_config and the scale_variant it is used with; fields of either read and write by name."""
+
+    _VARIANT = {name for name, _ in scale_variant._fields_}
+
+    def __init__(self, base: scale_config, variant: scale_variant):
+        object.__setattr__(self, "base", base)
+        object.__setattr__(self, "variant", variant)
+
+    def __getattr__(self, name):
+        return getattr(self.variant if name in Config._VARIANT else self.base, name)
+
+    def __setattr__(self, name, value):
+        setattr(self.variant if name in Config._VARIANT else self.base, name, value)
 
 
 def _load():
@@ -67,21 +89,27 @@ def _load():
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.scale_init.argtypes = [ctypes.POINTER(scale_config), vp, ctypes.POINTER(vp)]
     lib.scale_init.restype = ctypes.c_int
+    lib.scale_init_variant.argtypes = [ctypes.POINTER(scale_config), ctypes.POINTER(scale_variant), vp,
+                                       ctypes.POINTER(vp)]
+    lib.scale_init_variant.restype = ctypes.c_int
     lib.scale_free.argtypes = [vp]
     lib.scale_free.restype = None
     lib.scale_rep_keys.argtypes = [vp, vp, vp, i32, vp]
     lib.scale_rep_keys.restype = ctypes.c_int
-    lib.scale_select_cluster.argtypes = [vp, vp, i32, vp, vp, i32, vp, vp, vp, vp]
+    lib.scale_select_cluster.argtypes = [vp, vp, i32, vp, vp, i32, vp, vp, vp]
     lib.scale_select_cluster.restype = ctypes.c_int
-    lib.scale_select_cluster_tokens.argtypes = [vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.scale_select_cluster_tokens.argtypes = [vp, vp, i32, vp, vp, vp, i32, vp, vp, vp]
     lib.scale_select_cluster_tokens.restype = ctypes.c_int
+    lib.scale_fingerprints.argtypes = [vp, vp, i32]
+    lib.scale_fingerprints.restype = ctypes.c_int
     lib.scale_sparse_prefill.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp]
     lib.scale_sparse_prefill.restype = ctypes.c_int
     lib.scale_status_string.argtypes = [ctypes.c_int]
     lib.scale_status_string.restype = ctypes.c_char_p
     lib.scale_retrieval_calls.argtypes = [vp, ctypes.POINTER(i64)]
     lib.scale_retrieval_calls.restype = ctypes.c_int
-    lib.scale_cluster_geometry.argtypes = [ctypes.POINTER(scale_config), i32, vp, i32, vp]
+    lib.scale_cluster_geometry.argtypes = [ctypes.POINTER(scale_config), ctypes.POINTER(scale_variant), i32, vp,
+                                           i32, vp]
     lib.scale_cluster_geometry.restype = ctypes.c_int
     lib.scale_enable_timing.argtypes = [vp, ctypes.c_int]
     lib.scale_enable_timing.restype = ctypes.c_int
@@ -125,19 +153,19 @@ def _cluster_start(cs) -> np.ndarray:
 def make_config(*, num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
                 local_window, max_tokens, max_clusters, softmax_scale=0.0, score_scale=0.0,
                 out_dtype=SCALE_OUT_F32, select_tokens=False, rep_kind=SCALE_REP_MEAN,
-                kv_head_sets=False) -> scale_config:
-    return scale_config(num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
-                        local_window, max_tokens, max_clusters, softmax_scale, score_scale, out_dtype,
-                        1 if select_tokens else 0, int(rep_kind), 1 if kv_head_sets else 0)
+                kv_head_sets=False) -> Config:
+    return Config(scale_config(num_q_heads, num_kv_heads, head_dim, block_size, sub_chunk, top_k, sink_tokens,
+                               local_window, max_tokens, max_clusters, softmax_scale, score_scale, out_dtype),
+                  scale_variant(1 if select_tokens else 0, int(rep_kind), 1 if kv_head_sets else 0))
 
 
-def scale_cluster_geometry(cfg: scale_config, n_tokens: int, cluster_start) -> np.ndarray:
+def scale_cluster_geometry(cfg: Config, n_tokens: int, cluster_start) -> np.ndarray:
     """Host-only geometry: int32 [n_clusters, 6] = (s, e, lo_blk, sink_eff, n_cand, sel_cnt)."""
     cs = _cluster_start(cluster_start)
     n = len(cs) - 1
     geo = np.zeros((max(n, 0), 6), dtype=np.int32)
-    _check(lib.scale_cluster_geometry(ctypes.byref(cfg), int(n_tokens), cs.ctypes.data, n, geo.ctypes.data),
-           "scale_cluster_geometry")
+    _check(lib.scale_cluster_geometry(ctypes.byref(cfg.base), ctypes.byref(cfg.variant), int(n_tokens),
+                                      cs.ctypes.data, n, geo.ctypes.data), "scale_cluster_geometry")
     return geo
 
 
@@ -154,11 +182,12 @@ def _stream_handle(stream):
 class Scale:
     """One library handle (scale_init ... scale_free), bound to the current device and a stream."""
 
-    def __init__(self, cfg: scale_config, stream=None):
+    def __init__(self, cfg: Config, stream=None):
         self.cfg = cfg
         self.stream = _stream_handle(stream)
         h = ctypes.c_void_p()
-        _check(lib.scale_init(ctypes.byref(cfg), self.stream, ctypes.byref(h)), "scale_init")
+        _check(lib.scale_init_variant(ctypes.byref(cfg.base), ctypes.byref(cfg.variant), self.stream,
+                                      ctypes.byref(h)), "scale_init_variant")
         self._h = h
 
     def close(self):
@@ -190,20 +219,22 @@ class Scale:
         _check(lib.scale_rep_keys_range(self._h, _ptr(k_pages), _ptr(block_table), int(first_block), int(n_tokens),
                                         _ptr(k_rep)), "scale_rep_keys_range")
 
-    def select_cluster(self, q, n_tokens: int, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None,
-                       fingerprints_out=None):
+    def select_cluster(self, q, n_tokens: int, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None):
         cs = _cluster_start(cluster_start)
         _check(lib.scale_select_cluster(self._h, _ptr(q), int(n_tokens), _ptr(k_rep), cs.ctypes.data, len(cs) - 1,
-                                        _ptr(sel_idx), _ptr(sel_cnt), _ptr(scores_out), _ptr(fingerprints_out)),
+                                        _ptr(sel_idx), _ptr(sel_cnt), _ptr(scores_out)),
                "scale_select_cluster")
 
     def select_cluster_tokens(self, q, n_tokens: int, k_pages, block_table, cluster_start, sel_idx, sel_cnt,
-                              scores_out=None, fingerprints_out=None):
+                              scores_out=None):
         cs = _cluster_start(cluster_start)
         _check(lib.scale_select_cluster_tokens(self._h, _ptr(q), int(n_tokens), _ptr(k_pages), _ptr(block_table),
                                                cs.ctypes.data, len(cs) - 1, _ptr(sel_idx), _ptr(sel_cnt),
-                                               _ptr(scores_out), _ptr(fingerprints_out)),
+                                               _ptr(scores_out)),
                "scale_select_cluster_tokens")
+
+    def fingerprints(self, out, n_clusters: int):
+        _check(lib.scale_fingerprints(self._h, _ptr(out), int(n_clusters)), "scale_fingerprints")
 
     def sparse_prefill(self, q, k_pages, v_pages, block_table, n_tokens: int, cluster_start, sel_idx, sel_cnt, out):
         cs = _cluster_start(cluster_start)
@@ -247,7 +278,7 @@ class Scale:
 
 
 # Same names as the C ABI, for callers that prefer the flat form.
-def scale_init(cfg: scale_config, stream=None) -> Scale:
+def scale_init(cfg: Config, stream=None) -> Scale:
     return Scale(cfg, stream)
 
 
@@ -259,19 +290,17 @@ def scale_rep_keys(h: Scale, k_pages, block_table, n_tokens, k_rep):
     h.rep_keys(k_pages, block_table, n_tokens, k_rep)
 
 
-def scale_select_cluster(h: Scale, q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None,
-                         fingerprints_out=None):
-    h.select_cluster(q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out, fingerprints_out)
+def scale_select_cluster(h: Scale, q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None):
+    h.select_cluster(q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out)
 
 
 def scale_select_cluster_tokens(h: Scale, q, n_tokens, k_pages, block_table, cluster_start, sel_idx, sel_cnt,
-                                scores_out=None, fingerprints_out=None):
-    h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cluster_start, sel_idx, sel_cnt, scores_out,
-                            fingerprints_out)
+                                scores_out=None):
+    h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cluster_start, sel_idx, sel_cnt, scores_out)
 
 
-def scale_sparse_prefill(h: Scale, q, k_pages, v_pages, block_table, n_tokens, cluster_start, sel_idx, sel_cnt, out):
-    h.sparse_prefill(q, k_pages, v_pages, block_table, n_tokens, cluster_start, sel_idx, sel_cnt, out)
+def scale_fingerprints(h: Scale, out, n_clusters):
+    h.fingerprints(out, n_clusters)
 
 
 def scale_retrieval_calls(h: Scale) -> int:

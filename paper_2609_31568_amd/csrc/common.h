@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "scale.h"
+
 namespace scale {
 
 // Geometry of one cluster as the kernels read it (see include/scale.h for the definitions).
@@ -28,6 +30,15 @@ struct WorkItem {
 };
 static_assert(sizeof(WorkItem) == 16, "WorkItem is uploaded as raw bytes");
 
+// ---- host validation and geometry (scale_api.cpp) ----
+
+// The configuration rules of scale_init_variant (no HIP call).
+scale_status validate_config(const scale_config* c, const scale_variant* v);
+// Validates n_tokens and cluster_start against the configuration (the rules of every per-layer
+// call, capacity included) and, when geo is not null, writes each cluster's geometry.
+scale_status plan_geometry(const scale_config& c, const scale_variant& v, int32_t n_tokens,
+                           const int32_t* cluster_start, int32_t n_clusters, ClusterGeo* geo);
+
 // ---- launchers (each defined next to its kernel) ----
 
 // k_rep[b][g][:] = mean over block b of K (fp64 accumulation, one rounding to fp32), or with
@@ -37,28 +48,32 @@ hipError_t launch_rep_keys(const uint16_t* k_pages, const int32_t* block_table, 
                            int num_kv_heads, int block_size, int head_dim, bool bounds, float* k_rep,
                            hipStream_t stream);
 
-// Anchor fingerprints: fp32 mean of each cluster's anchor rows (fp64 sums).
+// Anchor fingerprints: mean of each cluster's anchor rows (fp64 sums), rounded once to fp32 into
+// `fingerprints` and, when fingerprints64 is not null, stored unrounded there too.
 hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
-                               int num_q_heads, int head_dim, float* fingerprints, hipStream_t stream);
+                               int num_q_heads, int head_dim, float* fingerprints, double* fingerprints64,
+                               hipStream_t stream);
 
-// Candidate chunks of the selection kernels for `max_cand` candidates; head_stats holds
-// n_clusters * Hq * selection_chunks(max_cand) (max, sum) pairs.
+// Candidate chunks of the selection kernels for `max_cand` candidates: the statistics and factor
+// scratch hold n_clusters * Hq * selection_chunks(max_cand) entries.
 int selection_chunks(int max_cand);
 
-// Selection logits x[j][h][c] for candidate c of cluster j (row stride `cand_stride`), and each
-// candidate chunk's softmax partials per head; `bounds` scores the channel-wise key bounds.
-hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
-                               int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, float score_scale,
-                               float* logits, float2* head_stats, hipStream_t stream);
+// fp64 selection logits of candidate c of cluster j per query head, reduced per 64-candidate chunk
+// k to the softmax partials stats[j][h][k] = (m, sum of exp(x - m)) and the weights
+// weights[j][h][c] = exp(x - m) (row stride `cand_stride`); `bounds` scores the channel-wise key
+// bounds.
+hipError_t launch_block_logits(const double* fingerprints, const float* k_rep, const ClusterGeo* geo,
+                               int n_clusters, int max_cand, int64_t cand_stride, int sink_blk,
+                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, double score_scale,
+                               double* weights, double2* stats, hipStream_t stream);
 
-// Soft-voting scores and deterministic top-k per cluster, or per (cluster, KV head) with
-// `per_kv` (output rows j * Hkv + g, each voted by the query heads of g).
-hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo,
-                            int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                            int num_q_heads, int num_kv_heads, bool per_kv, int top_k, int n_blocks,
-                            float* spill, int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
-                            hipStream_t stream);
+// Soft-voting scores (fp64, rounded once to fp32) and deterministic top-k per cluster, or per
+// (cluster, KV head) with `per_kv` (output rows j * Hkv + g, each voted by the query heads of g).
+// `factors` is scratch of the size of the statistics.
+hipError_t launch_vote_topk(const double* weights, const double2* stats, double* factors, const ClusterGeo* geo,
+                            int n_clusters, int max_cand, int64_t cand_stride, int sink_blk, int num_q_heads,
+                            int num_kv_heads, bool per_kv, int top_k, int n_blocks, float* spill, int32_t* sel_idx,
+                            int32_t* sel_cnt, float* scores_out, hipStream_t stream);
 
 // Sub-chunk similarity for the anchor-based clustering of sub-chunks [first, M), M =
 // ceil(n_tokens / sub_chunk), indexed from first: fp64 fingerprints [M - first][Hq * d], their

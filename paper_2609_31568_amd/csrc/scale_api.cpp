@@ -39,17 +39,22 @@ struct TimedLaunch {
 
 struct scale_ctx {
   scale_config cfg{};
+  scale_variant var{};
   hipStream_t stream = nullptr;
   int device = 0;
   int64_t retrieval_calls = 0;
   int max_blocks = 0;        // max_tokens / B (rounded up)
   int max_items = 0;
+  int last_clusters = 0;     // clusters of the most recent selection call (its fingerprints)
   // device scratch
   ClusterGeo* d_geo = nullptr;
   WorkItem* d_items = nullptr;
-  float2* d_head_stats = nullptr;
   float* d_fingerprints = nullptr;
-  float* d_logits = nullptr;
+  // block-level selection: fp64 fingerprints, per-chunk weights and softmax partials, chunk factors
+  double* d_fp64 = nullptr;
+  double* d_weights = nullptr;
+  double2* d_stats = nullptr;
+  double* d_factors = nullptr;
   float* d_spill = nullptr;
   // sub-chunk clustering: fp64 fingerprints, inverse norms, cosine band (device) and the band's
   // pinned host copy
@@ -61,6 +66,8 @@ struct scale_ctx {
   // token-level selection (select_tokens): fingerprint pieces, chunk statistics, log-normalisers,
   // per-KV-head partial scores, the score rows of the top-k, and the gathered keys / values
   int kpad = 0;              // top_k rounded up to a whole gathered tile
+  int64_t tok_stride = 0;    // row stride of the partial scores and score rows: max_tokens rounded up to
+                             // a whole token tile, so every row starts 256-byte aligned
   uint16_t* d_tok_F = nullptr;
   float2* d_tok_stats = nullptr;
   float* d_tok_lse = nullptr;
@@ -83,8 +90,12 @@ struct scale_ctx {
 
 namespace {
 
-scale_status validate_config(const scale_config* c) {
-  if (!c) return SCALE_ERR_INVALID_ARG;
+}  // namespace
+
+namespace scale {
+
+scale_status validate_config(const scale_config* c, const scale_variant* v) {
+  if (!c || !v) return SCALE_ERR_INVALID_ARG;
   if (c->num_q_heads < 1 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads) return SCALE_ERR_INVALID_ARG;
   if (c->head_dim < 1 || c->block_size < 1 || c->sub_chunk < 1) return SCALE_ERR_INVALID_ARG;
   if (c->top_k < 0 || c->sink_tokens < 0 || c->local_window < 0) return SCALE_ERR_INVALID_ARG;
@@ -92,17 +103,17 @@ scale_status validate_config(const scale_config* c) {
   if (!std::isfinite(c->softmax_scale) || c->softmax_scale < 0.f) return SCALE_ERR_INVALID_ARG;
   if (!std::isfinite(c->score_scale)) return SCALE_ERR_INVALID_ARG;
   if (c->out_dtype != SCALE_OUT_F32 && c->out_dtype != SCALE_OUT_BF16) return SCALE_ERR_INVALID_ARG;
-  if (c->select_tokens != 0 && c->select_tokens != 1) return SCALE_ERR_INVALID_ARG;
-  if (c->rep_kind != SCALE_REP_MEAN && c->rep_kind != SCALE_REP_BOUNDS) return SCALE_ERR_INVALID_ARG;
-  if (c->kv_head_sets != 0 && c->kv_head_sets != 1) return SCALE_ERR_INVALID_ARG;
-  if (c->select_tokens && c->rep_kind == SCALE_REP_BOUNDS) return SCALE_ERR_UNSUPPORTED;   // tokens use their keys
+  if (v->select_tokens != 0 && v->select_tokens != 1) return SCALE_ERR_INVALID_ARG;
+  if (v->rep_kind != SCALE_REP_MEAN && v->rep_kind != SCALE_REP_BOUNDS) return SCALE_ERR_INVALID_ARG;
+  if (v->kv_head_sets != 0 && v->kv_head_sets != 1) return SCALE_ERR_INVALID_ARG;
+  if (v->select_tokens && v->rep_kind == SCALE_REP_BOUNDS) return SCALE_ERR_UNSUPPORTED;   // tokens use their keys
   if (c->head_dim != 64 && c->head_dim != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->block_size != 64 && c->block_size != 128) return SCALE_ERR_UNSUPPORTED;
   if (c->sub_chunk % c->block_size) return SCALE_ERR_UNSUPPORTED;
   if (c->num_q_heads / c->num_kv_heads > 8) return SCALE_ERR_UNSUPPORTED;
   // sizes that keep every int32 index of the kernels in range
   if ((int64_t)c->max_tokens * c->num_q_heads * c->head_dim >= ((int64_t)1 << 40)) return SCALE_ERR_UNSUPPORTED;
-  if (c->select_tokens) {
+  if (v->select_tokens) {
     // gathered rows and token-scoring rows are int32 indices in the kernels
     const int64_t kpad = ((int64_t)c->top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
     if ((int64_t)c->max_clusters * c->num_kv_heads * kpad >= ((int64_t)1 << 31)) return SCALE_ERR_UNSUPPORTED;
@@ -112,8 +123,8 @@ scale_status validate_config(const scale_config* c) {
 }
 
 // Validates n_tokens and cluster_start against the config; fills the geometry when geo != null.
-scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_t* cluster_start,
-                           int32_t n_clusters, ClusterGeo* geo) {
+scale_status plan_geometry(const scale_config& c, const scale_variant& v, int32_t n_tokens,
+                           const int32_t* cluster_start, int32_t n_clusters, ClusterGeo* geo) {
   if (!cluster_start || n_clusters < 1 || n_tokens < 1) return SCALE_ERR_INVALID_ARG;
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens || n_clusters > c.max_clusters) return SCALE_ERR_CAPACITY;
@@ -132,12 +143,19 @@ scale_status plan_geometry(const scale_config& c, int32_t n_tokens, const int32_
     const int lo = std::max(0, std::min(g.s, g.e - c.local_window));
     g.lo_blk = lo / B;
     g.sink_eff = std::min(sink_blk, g.lo_blk);
-    g.n_cand = std::max(0, g.lo_blk - sink_blk) * (c.select_tokens ? B : 1);
+    g.n_cand = std::max(0, g.lo_blk - sink_blk) * (v.select_tokens ? B : 1);
     g.sel_cnt = std::min(c.top_k, g.n_cand);
     g.pad = 0;
   }
   return SCALE_OK;
 }
+
+}  // namespace scale
+
+namespace {
+
+using scale::plan_geometry;
+using scale::validate_config;
 
 int64_t max_work_items(const scale_config& c) {
   const int64_t tiles = ((int64_t)c.max_tokens + scale::kTilePositions - 1) / scale::kTilePositions + c.max_clusters;
@@ -186,9 +204,11 @@ void release(scale_ctx* h) {
   }
   (void)hipFree(h->d_geo);
   (void)hipFree(h->d_items);
-  (void)hipFree(h->d_head_stats);
   (void)hipFree(h->d_fingerprints);
-  (void)hipFree(h->d_logits);
+  (void)hipFree(h->d_fp64);
+  (void)hipFree(h->d_weights);
+  (void)hipFree(h->d_stats);
+  (void)hipFree(h->d_factors);
   (void)hipFree(h->d_spill);
   (void)hipFree(h->d_sub_fp);
   (void)hipFree(h->d_inv_norm);
@@ -243,15 +263,16 @@ const char* scale_status_string(scale_status s) {
   return "unknown status";
 }
 
-scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens, const int32_t* cluster_start,
-                                    int32_t n_clusters, int32_t* geo_out) {
-  scale_status st = validate_config(cfg);
+scale_status scale_cluster_geometry(const scale_config* cfg, const scale_variant* variant, int32_t n_tokens,
+                                    const int32_t* cluster_start, int32_t n_clusters, int32_t* geo_out) {
+  const scale_variant var = variant ? *variant : scale_variant{};
+  scale_status st = validate_config(cfg, &var);
   if (st != SCALE_OK) return st;
   if (!geo_out) return SCALE_ERR_INVALID_ARG;
-  st = plan_geometry(*cfg, n_tokens, cluster_start, n_clusters, nullptr);
+  st = plan_geometry(*cfg, var, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
   std::vector<ClusterGeo> geo(n_clusters);
-  plan_geometry(*cfg, n_tokens, cluster_start, n_clusters, geo.data());
+  plan_geometry(*cfg, var, n_tokens, cluster_start, n_clusters, geo.data());
   for (int j = 0; j < n_clusters; ++j) {
     const ClusterGeo& g = geo[j];
     int32_t* o = geo_out + 6 * j;
@@ -261,17 +282,25 @@ scale_status scale_cluster_geometry(const scale_config* cfg, int32_t n_tokens, c
 }
 
 scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle* out) {
+  return scale_init_variant(cfg, nullptr, hip_stream, out);
+}
+
+scale_status scale_init_variant(const scale_config* cfg, const scale_variant* variant, void* hip_stream,
+                                scale_handle* out) {
   if (!out) return SCALE_ERR_INVALID_ARG;
   *out = nullptr;
-  scale_status st = validate_config(cfg);
+  const scale_variant var = variant ? *variant : scale_variant{};
+  scale_status st = validate_config(cfg, &var);
   if (st != SCALE_OK) return st;
 
   scale_ctx* h = new (std::nothrow) scale_ctx();
   if (!h) return SCALE_ERR_OUT_OF_MEMORY;
   h->cfg = *cfg;
+  h->var = var;
   h->stream = reinterpret_cast<hipStream_t>(hip_stream);
   if (hipGetDevice(&h->device) != hipSuccess) { release(h); return SCALE_ERR_HIP; }
   const scale_config& c = h->cfg;
+  const scale_variant& v = h->var;
   h->max_blocks = (c.max_tokens + c.block_size - 1) / c.block_size;
   h->max_subchunks = (c.max_tokens + c.sub_chunk - 1) / c.sub_chunk;
   h->max_items = (int)max_work_items(c);
@@ -282,28 +311,34 @@ scale_status scale_init(const scale_config* cfg, void* hip_stream, scale_handle*
     if (bytes == 0) return true;
     return hipMalloc(p, bytes) == hipSuccess;
   };
+  const int64_t chunk_entries = mc * c.num_q_heads * scale::selection_chunks(h->max_blocks);
+  const bool blocks = !v.select_tokens;
   bool ok = dev((void**)&h->d_geo, sizeof(ClusterGeo) * mc) &&
             dev((void**)&h->d_items, sizeof(WorkItem) * (size_t)h->max_items) &&
-            dev((void**)&h->d_head_stats, sizeof(float2) * mc * c.num_q_heads * scale::selection_chunks(h->max_blocks)) &&
             dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
-            dev((void**)&h->d_logits, sizeof(float) * mc * c.num_q_heads * (int64_t)h->max_blocks) &&
-            dev((void**)&h->d_spill,
-                h->max_blocks > 8192 ? sizeof(float) * mc * (c.kv_head_sets ? c.num_kv_heads : 1) * h->max_blocks : 0) &&
+            dev((void**)&h->d_fp64, blocks ? sizeof(double) * mc * row_elems : 0) &&
+            dev((void**)&h->d_weights, blocks ? sizeof(double) * mc * c.num_q_heads * (int64_t)h->max_blocks : 0) &&
+            dev((void**)&h->d_stats, blocks ? sizeof(double2) * chunk_entries : 0) &&
+            dev((void**)&h->d_factors, blocks ? sizeof(double) * chunk_entries : 0) &&
+            dev((void**)&h->d_spill, blocks && h->max_blocks > 8192
+                                         ? sizeof(float) * mc * (v.kv_head_sets ? c.num_kv_heads : 1) * h->max_blocks
+                                         : 0) &&
             dev((void**)&h->d_sub_fp, sizeof(double) * (size_t)h->max_subchunks * row_elems) &&
             dev((void**)&h->d_inv_norm, sizeof(double) * (size_t)h->max_subchunks) &&
             dev((void**)&h->d_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan) &&
             hipHostMalloc((void**)&h->h_band, sizeof(double) * (size_t)h->max_subchunks * scale::kMaxClusterSpan,
                           hipHostMallocDefault) == hipSuccess;
-  if (ok && c.select_tokens) {
+  if (ok && v.select_tokens) {
     const int group = c.num_q_heads / c.num_kv_heads;
     const int64_t rows = (int64_t)c.num_kv_heads * scale::token_row_pad(c.max_clusters, group);
     h->kpad = (c.top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
+    h->tok_stride = ((int64_t)c.max_tokens + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
     const int64_t gathered = mc * c.num_kv_heads * h->kpad * c.head_dim;
     ok = dev((void**)&h->d_tok_F, sizeof(uint16_t) * rows * 2 * c.head_dim) &&
          dev((void**)&h->d_tok_stats, sizeof(float2) * rows * scale::token_chunks(c.max_tokens)) &&
          dev((void**)&h->d_tok_lse, sizeof(float) * rows) &&
-         dev((void**)&h->d_tok_partial, sizeof(float) * mc * c.num_kv_heads * (int64_t)c.max_tokens) &&
-         dev((void**)&h->d_tok_score, sizeof(float) * mc * (int64_t)c.max_tokens) &&
+         dev((void**)&h->d_tok_partial, sizeof(float) * mc * c.num_kv_heads * h->tok_stride) &&
+         dev((void**)&h->d_tok_score, sizeof(float) * mc * h->tok_stride) &&
          dev((void**)&h->d_gk, sizeof(uint16_t) * gathered) && dev((void**)&h->d_gv, sizeof(uint16_t) * gathered);
   }
   if (!ok) {
@@ -336,6 +371,14 @@ scale_status scale_retrieval_calls(scale_handle h, int64_t* calls) {
   return SCALE_OK;
 }
 
+scale_status scale_fingerprints(scale_handle h, float* fingerprints, int32_t n_clusters) {
+  if (!h || !fingerprints || n_clusters < 1 || n_clusters > h->last_clusters) return SCALE_ERR_INVALID_ARG;
+  const size_t bytes = sizeof(float) * (size_t)n_clusters * h->cfg.num_q_heads * h->cfg.head_dim;
+  return hipMemcpyAsync(fingerprints, h->d_fingerprints, bytes, hipMemcpyDeviceToDevice, h->stream) == hipSuccess
+             ? SCALE_OK
+             : SCALE_ERR_HIP;
+}
+
 scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32_t* block_table, int32_t n_tokens,
                             float* k_rep) {
   if (!h || !k_pages || !k_rep || n_tokens < 1) return SCALE_ERR_INVALID_ARG;
@@ -344,7 +387,7 @@ scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
   stage_begin(h);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, 0, n_tokens / c.block_size, c.num_kv_heads,
-                                              c.block_size, c.head_dim, c.rep_kind == SCALE_REP_BOUNDS, k_rep,
+                                              c.block_size, c.head_dim, h->var.rep_kind == SCALE_REP_BOUNDS, k_rep,
                                               h->stream);
   stage_end(h, SCALE_STAGE_REP_KEYS);
   return check_launch(e);
@@ -359,7 +402,7 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
   if (first_block > n_tokens / c.block_size) return SCALE_ERR_INVALID_ARG;
   stage_begin(h);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, first_block, n_tokens / c.block_size,
-                                              c.num_kv_heads, c.block_size, c.head_dim, c.rep_kind == SCALE_REP_BOUNDS,
+                                              c.num_kv_heads, c.block_size, c.head_dim, h->var.rep_kind == SCALE_REP_BOUNDS,
                                               k_rep, h->stream);
   stage_end(h, SCALE_STAGE_REP_KEYS);
   return check_launch(e);
@@ -367,40 +410,42 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
 
 scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens, const float* k_rep,
                                   const int32_t* cluster_start, int32_t n_clusters, int32_t* sel_idx,
-                                  int32_t* sel_cnt, float* scores_out, float* fingerprints_out) {
+                                  int32_t* sel_cnt, float* scores_out) {
   if (!h || !q || !k_rep || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
-  if (c.select_tokens) return SCALE_ERR_UNSUPPORTED;
-  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  const scale_variant& v = h->var;
+  if (v.select_tokens) return SCALE_ERR_UNSUPPORTED;
+  scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
   Slot* slot = nullptr;
   if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
   ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
-  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
   int max_cand = 0;
   for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
   if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
 
   const int n_blocks = n_tokens / c.block_size;
   const int sink_blk = (c.sink_tokens + c.block_size - 1) / c.block_size;
-  const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
-  float* fps = fingerprints_out ? fingerprints_out : h->d_fingerprints;
+  const double sigma = c.score_scale == 0.f ? 1.0 : (double)c.score_scale;
   stage_begin(h);
-  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, h->stream));
+  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, h->d_fingerprints,
+                                               h->d_fp64, h->stream));
   stage_end(h, SCALE_STAGE_FINGERPRINT);
   if (st != SCALE_OK) return st;
+  h->last_clusters = n_clusters;
   stage_begin(h);
-  st = check_launch(scale::launch_block_logits(fps, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks, sink_blk,
-                                               c.num_q_heads, c.num_kv_heads, c.head_dim,
-                                               c.rep_kind == SCALE_REP_BOUNDS, sigma, h->d_logits, h->d_head_stats,
+  st = check_launch(scale::launch_block_logits(h->d_fp64, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks,
+                                               sink_blk, c.num_q_heads, c.num_kv_heads, c.head_dim,
+                                               v.rep_kind == SCALE_REP_BOUNDS, sigma, h->d_weights, h->d_stats,
                                                h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
   stage_begin(h);
-  st = check_launch(scale::launch_vote_topk(h->d_logits, h->d_head_stats, h->d_geo, n_clusters, max_cand,
+  st = check_launch(scale::launch_vote_topk(h->d_weights, h->d_stats, h->d_factors, h->d_geo, n_clusters, max_cand,
                                             h->max_blocks, sink_blk, c.num_q_heads, c.num_kv_heads,
-                                            c.kv_head_sets != 0, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
+                                            v.kv_head_sets != 0, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
                                             scores_out, h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
   if (st != SCALE_OK) return st;
@@ -410,39 +455,41 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
 
 scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens, const uint16_t* k_pages,
                                          const int32_t* block_table, const int32_t* cluster_start, int32_t n_clusters,
-                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out,
-                                         float* fingerprints_out) {
+                                         int32_t* sel_idx, int32_t* sel_cnt, float* scores_out) {
   if (!h || !q || !k_pages || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
-  if (!c.select_tokens) return SCALE_ERR_UNSUPPORTED;
-  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  const scale_variant& v = h->var;
+  if (!v.select_tokens) return SCALE_ERR_UNSUPPORTED;
+  scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
   Slot* slot = nullptr;
   if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
   ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
-  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
   int max_cand = 0;
   for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
   if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
 
   const int first_token = (c.sink_tokens + c.block_size - 1) / c.block_size * c.block_size;
   const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
-  float* fps = fingerprints_out ? fingerprints_out : h->d_fingerprints;
+  float* fps = h->d_fingerprints;
   stage_begin(h);
-  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, h->stream));
+  st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, nullptr,
+                                               h->stream));
   stage_end(h, SCALE_STAGE_FINGERPRINT);
   if (st != SCALE_OK) return st;
+  h->last_clusters = n_clusters;
   stage_begin(h);
   st = check_launch(scale::launch_token_selection(fps, k_pages, block_table, h->d_geo, n_clusters, max_cand,
                                                   first_token, c.num_q_heads, c.num_kv_heads, c.head_dim,
-                                                  c.block_size, sigma, c.max_tokens, h->d_tok_F, h->d_tok_stats,
+                                                  c.block_size, sigma, h->tok_stride, h->d_tok_F, h->d_tok_stats,
                                                   h->d_tok_lse, h->d_tok_partial, h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
   stage_begin(h);
-  st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, c.max_tokens, max_cand,
-                                                   first_token, c.num_kv_heads, c.kv_head_sets != 0, c.top_k,
+  st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, h->tok_stride, max_cand,
+                                                   first_token, c.num_kv_heads, v.kv_head_sets != 0, c.top_k,
                                                    n_tokens, h->d_tok_score, sel_idx, sel_cnt, scores_out,
                                                    h->stream));
   stage_end(h, SCALE_STAGE_VOTE_TOPK);
@@ -513,13 +560,14 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
                                   int32_t n_clusters, const int32_t* sel_idx, const int32_t* sel_cnt, void* out) {
   if (!h || !q || !k_pages || !v_pages || !sel_idx || !sel_cnt || !out) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
-  scale_status st = plan_geometry(c, n_tokens, cluster_start, n_clusters, nullptr);
+  const scale_variant& v = h->var;
+  scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
   Slot* slot = nullptr;
   if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
   ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
-  plan_geometry(c, n_tokens, cluster_start, n_clusters, geo);
+  plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
   WorkItem* items = reinterpret_cast<WorkItem*>(geo + n_clusters);
 
   // Work list. Clusters in order; inside a cluster, position tiles from the last (most keys) to
@@ -556,18 +604,18 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
 
   const float scale = c.softmax_scale == 0.f ? 1.0f / std::sqrt((float)c.head_dim) : c.softmax_scale;
   const float qk_scale_log2 = scale * 1.4426950408889634f;
-  const bool tokens = c.select_tokens && h->kpad > 0;
+  const bool tokens = v.select_tokens && h->kpad > 0;
   if (tokens) {
     stage_begin(h);
     st = check_launch(scale::launch_gather_selected(k_pages, v_pages, block_table, sel_idx, sel_cnt,
-                                                    c.kv_head_sets != 0, n_clusters, c.top_k, h->kpad, n_tokens,
+                                                    v.kv_head_sets != 0, n_clusters, c.top_k, h->kpad, n_tokens,
                                                     c.num_kv_heads, c.head_dim, B, h->d_gk, h->d_gv, h->stream));
     stage_end(h, SCALE_STAGE_GATHER);
     if (st != SCALE_OK) return st;
   }
   stage_begin(h);
   const hipError_t e = scale::launch_sparse_attention(
-      q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, c.kv_head_sets != 0,
+      q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, v.kv_head_sets != 0,
       c.top_k, c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
       c.out_dtype == SCALE_OUT_BF16, out, tokens ? h->d_gk : nullptr, tokens ? h->d_gv : nullptr, h->kpad,
       h->stream);

@@ -2,20 +2,26 @@
 // deterministic top-k, once per cluster (paper Sec. 5.1.3, Eq. 9 and the head soft-voting
 // instantiation of the selection function).
 //
-//  fingerprint   (column slice, cluster) -> fp32 mean of the anchor rows (fp64 sums)
-//  block_logits  (cluster, candidate chunks, KV head) -> x[h][c] = sigma * v[h] . k_rep[c][g(h)]
-//                for the query heads h of KV head g (bound form: sigma * sum_i max(v_i mn_i,
-//                v_i mx_i) over the block's channel-wise key bounds), plus each chunk's softmax
-//                partials (max_c x[h][c], sum_c exp(x[h][c] - max)) per head
-//  vote_topk     cluster (or (cluster, KV head) with one set per KV head) -> per-head softmax
-//                normaliser from the chunk partials, score = sum over the voting heads of the
-//                softmax weights, top-k by (score desc, index asc), ascending; token mode takes
-//                the scores of the token scoring kernels (select_tokens.hip)
+//  fingerprint   (column slice, cluster) -> mean of the anchor rows: fp64 sums, written in fp64
+//                (for the logits) and rounded once to fp32 (for token scoring and the caller)
+//  block_logits  (candidate tile, fingerprint-row tile, KV head) -> for the 64 rows (cluster j,
+//                query head h of KV head g) x 64 candidates c of the tile, the fp64 logit
+//                x = sigma * v[j][h] . k_rep[c][g] (bound form: sigma * sum_i max(v_i mn_i, v_i mx_i)),
+//                then per row the tile's softmax partials: m = max_c x, the weights exp(x - m) and
+//                their sum. A tile is one 64-candidate chunk; the k_rep tile staged in LDS serves
+//                every cluster whose rows share the tile (up to 64 clusters), the fingerprint tile
+//                every candidate of it
+//  vote_topk     cluster (or (cluster, KV head) with one set per KV head) -> per head the softmax
+//                maximum and normaliser from the chunk partials and one factor exp(m_k - M) / S per
+//                chunk, score = sum over the voting heads of weight x factor (all fp64), rounded
+//                once to fp32; top-k by (score desc, index asc), ascending; token mode takes the
+//                scores of the token scoring kernels (select_tokens.hip)
 //  token_sum     (candidate slice, cluster) -> token scores: the per-KV-head partial scores summed
 //                in KV-head order
 //
-// All of it is HBM/L2-bandwidth work (a few FLOP per byte); every reduction has a fixed order,
-// so two runs give identical bits.
+// The softmax of a head is split exactly: exp(x - M) / S = exp(x - m_k) * exp(m_k - M) / S for
+// the chunk k holding x, with S = sum_k s_k exp(m_k - M). Every reduction has a fixed order, so two
+// runs give identical bits.
 #include <float.h>
 
 #include <algorithm>
@@ -29,15 +35,17 @@ constexpr int kThreads = 256;
 constexpr int kFpThreads = 512;          // fingerprint: 8 waves
 constexpr int kFpCols = 512;             // columns of the Hq*d row per fingerprint work-group
 constexpr int kFpRowsInFlight = 4;       // 16-byte loads in flight per lane
-constexpr int kCandChunk = 64;           // candidates per block_logits step
-constexpr int kLogitsTargetGroups = 4096;
+constexpr int kCandChunk = 64;           // candidates per logits tile = per softmax-partial chunk
+constexpr int kLgRows = 64;              // fingerprint rows (cluster, query head) per logits tile
+constexpr int kLgDk = 32;                // head-dim slice staged in LDS per step
 
 // grid: (column slice, cluster). Lane l of wave w owns the 8 columns [slice*512 + 8l, +8) and
 // sums anchor rows w, w+8, w+16, ... in fp64 (exact for bf16 inputs of moderate range); the 8
 // waves' sums are combined in LDS in wave order and divided once.
 __global__ __launch_bounds__(kFpThreads) void fingerprint_kernel(const uint16_t* __restrict__ q,
                                                                  const ClusterGeo* __restrict__ geo,
-                                                                 int row_elems, float* __restrict__ fingerprints) {
+                                                                 int row_elems, float* __restrict__ fingerprints,
+                                                                 double* __restrict__ fingerprints64) {
   constexpr int kWaves = kFpThreads / 64;
   __shared__ double part[kWaves][kFpCols];
   const int j = blockIdx.y;
@@ -77,108 +85,148 @@ __global__ __launch_bounds__(kFpThreads) void fingerprint_kernel(const uint16_t*
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) s += part[w][threadIdx.x];
-    fingerprints[(int64_t)j * row_elems + c] = (float)(s / (double)n_rows);
+    const double mean = s / (double)n_rows;
+    fingerprints[(int64_t)j * row_elems + c] = (float)mean;
+    if (fingerprints64) fingerprints64[(int64_t)j * row_elems + c] = mean;
   }
 }
 
-// grid: linear over (cluster j, part p, KV head g) with g fastest: work-groups are handed to the
-// 8 XCDs round-robin, so one XCD reads one KV head's slice of k_rep from its own L2. The work-group
-// takes candidate chunks p, p + parts, ... of cluster j. In a chunk, wave w holds candidates
-// [16w, 16w + 16) with four lanes per candidate; lane quarter q loads the float4s {4i + q} of the
-// candidate's representative key (64 contiguous bytes per candidate per load), forms partial dot
-// products with the fingerprints of the (at most 8) query heads of g held in LDS, and the four
-// lanes add their partials.
+// grid: linear over (candidate tile ct, row tile rt, KV head g), g fastest, so the 8 XCDs each
+// serve KV heads of their own (one KV head's slice of k_rep per L2 when Hkv = 8). Rows of KV head g
+// are r = j * G + u (cluster j, query head g * G + u); a work-group takes rows [64 rt, 64 rt + 64)
+// and candidates [64 ct, 64 ct + 64) and skips the tile when no cluster of its rows has that many
+// candidates. 256 threads as 16 x 16: thread (tr, tc) owns rows 4 tr .. 4 tr + 3 and candidates
+// 4 tc .. 4 tc + 3 (tc in the low lane bits, so a row's 16 threads are 16 consecutive lanes). The
+// head dim is staged through LDS in slices of 32, fingerprints and keys both as doubles stored
+// [dim][row or candidate], so each step reads 4 fingerprint and 4 key values and does 16 fp64 fmas.
 template <int D, bool kBounds>
 __global__ __launch_bounds__(kThreads) void block_logits_kernel(
-    const float* __restrict__ fingerprints, const float* __restrict__ k_rep,
-    const ClusterGeo* __restrict__ geo, int parts, int n_chunks, int cand_stride, int sink_blk,
-    int num_q_heads, int num_kv_heads, float score_scale, float* __restrict__ logits,
-    float2* __restrict__ head_stats) {
-  constexpr int kVec = D / 16;                      // float4 loads per lane
-  __shared__ float4 v_lds[8 * D / 4];               // fingerprints of the query heads of g
-  __shared__ float red[kThreads / 64][8];
+    const double* __restrict__ fingerprints, const float* __restrict__ k_rep, const ClusterGeo* __restrict__ geo,
+    int n_clusters, int row_tiles, int n_chunks, int64_t cand_stride, int sink_blk, int num_q_heads,
+    int num_kv_heads, double score_scale, double* __restrict__ weights, double2* __restrict__ stats) {
+  constexpr int kKeys = kBounds ? 2 : 1;                  // mean key, or minima then maxima
+  __shared__ double v_lds[kLgDk][kLgRows];
+  __shared__ double k_lds[kKeys][kLgDk][kCandChunk];
+  const int G = num_q_heads / num_kv_heads;
   const int g = blockIdx.x % num_kv_heads;
   const int rest = blockIdx.x / num_kv_heads;
-  const int p = rest % parts;
-  const int j = rest / parts;
-  const ClusterGeo G = geo[j];
-  const int chunks = (G.n_cand + kCandChunk - 1) / kCandChunk;
-  if (p >= chunks) return;                          // uniform over the work-group
-  const int group = num_q_heads / num_kv_heads;     // <= 8
-  const float4* vsrc = reinterpret_cast<const float4*>(fingerprints + ((int64_t)j * num_q_heads + g * group) * D);
-  for (int i = threadIdx.x; i < group * D / 4; i += kThreads) v_lds[i] = vsrc[i];
-  __syncthreads();
-  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  const int q4 = lane & 3;
-  for (int chunk = p; chunk < chunks; chunk += parts) {
-    const int c = chunk * kCandChunk + wave * 16 + lane / 4;
-    const bool valid = c < G.n_cand;
-    float4 kv[kVec], kx[kBounds ? kVec : 1];
-    const float4* kr = reinterpret_cast<const float4*>(
-        k_rep + ((int64_t)(sink_blk + (valid ? c : 0)) * num_kv_heads + g) * (kBounds ? 2 * D : D));
+  const int rt = rest % row_tiles;
+  const int ct = rest / row_tiles;
+  const int n_rows = n_clusters * G;
+  const int r0 = rt * kLgRows, c0 = ct * kCandChunk;
+  const int tid = threadIdx.x, lane = tid % 64;
+
+  // candidates of the tile's clusters (at most 64 clusters: one per lane), reduced per wave
+  const int j_first = r0 / G, j_last = (min(n_rows, r0 + kLgRows) - 1) / G;
+  int nc = 0;
+  if (j_first + lane <= j_last) nc = geo[j_first + lane].n_cand;
 #pragma unroll
-    for (int i = 0; i < kVec; ++i) kv[i] = kr[4 * i + q4];               // mean, or the minima
-    if constexpr (kBounds) {
+  for (int o = 1; o < 64; o <<= 1) nc = max(nc, __shfl_xor(nc, o, 64));
+  if (c0 >= nc) return;                                   // uniform over the work-group
+
+  const int tr = tid / 16, tc = tid % 16;
+  // staging: thread t loads 8 consecutive dims of row / candidate t / 4
+  const int ld_row = tid / 4, ld_part = (tid % 4) * 8;
+  const int r_ld = r0 + ld_row;
+  const double* v_src = nullptr;
+  if (r_ld < n_rows)
+    v_src = fingerprints + ((int64_t)(r_ld / G) * num_q_heads + g * G + r_ld % G) * D + ld_part;
+  const int c_ld = c0 + ld_row;
+  const float* k_src = nullptr;
+  if (c_ld < nc) k_src = k_rep + ((int64_t)(sink_blk + c_ld) * num_kv_heads + g) * (kKeys * D) + ld_part;
+
+  double acc[4][4];
 #pragma unroll
-      for (int i = 0; i < kVec; ++i) kx[i] = kr[D / 4 + 4 * i + q4];    // the maxima
-    }
-    float x[8];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      x[u] = 0.f;
-      if (u < group) {
-        float acc = 0.f;
+    for (int q = 0; q < 4; ++q) acc[i][q] = 0.0;
+
+  for (int d0 = 0; d0 < D; d0 += kLgDk) {
+    {
+      double vv[8];
+      float kk[kKeys][8];
 #pragma unroll
-        for (int i = 0; i < kVec; ++i) {
-          const float4 v = v_lds[u * (D / 4) + 4 * i + q4];
-          if constexpr (kBounds) {
-            acc += fmaxf(v.x * kv[i].x, v.x * kx[i].x);
-            acc += fmaxf(v.y * kv[i].y, v.y * kx[i].y);
-            acc += fmaxf(v.z * kv[i].z, v.z * kx[i].z);
-            acc += fmaxf(v.w * kv[i].w, v.w * kx[i].w);
-          } else {
-            acc = fmaf(v.x, kv[i].x, acc);
-            acc = fmaf(v.y, kv[i].y, acc);
-            acc = fmaf(v.z, kv[i].z, acc);
-            acc = fmaf(v.w, kv[i].w, acc);
-          }
-        }
-        acc += __shfl_xor(acc, 1, 64);
-        acc += __shfl_xor(acc, 2, 64);
-        x[u] = score_scale * acc;
-        if (valid && q4 == (u & 3))
-          logits[((int64_t)j * num_q_heads + g * group + u) * cand_stride + c] = x[u];
+      for (int e = 0; e < 8; e += 2) {
+        const double2 t = v_src ? *reinterpret_cast<const double2*>(v_src + d0 + e) : make_double2(0.0, 0.0);
+        vv[e] = t.x;
+        vv[e + 1] = t.y;
       }
+#pragma unroll
+      for (int m = 0; m < kKeys; ++m)
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+          const float4 t = k_src ? *reinterpret_cast<const float4*>(k_src + m * D + d0 + e)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+          kk[m][e] = t.x;
+          kk[m][e + 1] = t.y;
+          kk[m][e + 2] = t.z;
+          kk[m][e + 3] = t.w;
+        }
+      __syncthreads();                                    // the previous slice has been read
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v_lds[ld_part + e][ld_row] = vv[e];
+#pragma unroll
+      for (int m = 0; m < kKeys; ++m)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) k_lds[m][ld_part + e][ld_row] = (double)kk[m][e];
+      __syncthreads();
     }
-    // softmax partials of this chunk per head: max over its candidates, then sum of exp(x - max)
-    float m[8];
+#pragma unroll 4
+    for (int dd = 0; dd < kLgDk; ++dd) {
+      const double2 va = *reinterpret_cast<const double2*>(&v_lds[dd][4 * tr]);
+      const double2 vb = *reinterpret_cast<const double2*>(&v_lds[dd][4 * tr + 2]);
+      const double v[4] = {va.x, va.y, vb.x, vb.y};
+      double k[kKeys][4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      float t = valid ? x[u] : -FLT_MAX;
+      for (int m = 0; m < kKeys; ++m) {
+        const double2 ka = *reinterpret_cast<const double2*>(&k_lds[m][dd][4 * tc]);
+        const double2 kb = *reinterpret_cast<const double2*>(&k_lds[m][dd][4 * tc + 2]);
+        k[m][0] = ka.x;
+        k[m][1] = ka.y;
+        k[m][2] = kb.x;
+        k[m][3] = kb.y;
+      }
 #pragma unroll
-      for (int o = 4; o < 64; o <<= 1) t = fmaxf(t, __shfl_xor(t, o, 64));
-      m[u] = t;
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if constexpr (kBounds)
+            acc[i][q] += fmax(v[i] * k[0][q], v[i] * k[1][q]);
+          else
+            acc[i][q] = fma(v[i], k[0][q], acc[i][q]);
+        }
     }
-    if (lane == 0)
-      for (int u = 0; u < group; ++u) red[wave][u] = m[u];
-    __syncthreads();
+  }
+
+  // per row: this tile's softmax partials over its valid candidates (16 lanes per row)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) m[u] = fmaxf(fmaxf(red[0][u], red[1][u]), fmaxf(red[2][u], red[3][u]));
-    __syncthreads();
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + 4 * tr + i;
+    const int j = r / G;
+    const int n_valid = r < n_rows ? geo[j].n_cand - c0 : 0;   // candidates of row r in this tile
+    double x[4], m = -DBL_MAX;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      float t = (valid && u < group) ? expf(x[u] - m[u]) : 0.f;
-#pragma unroll
-      for (int o = 4; o < 64; o <<= 1) t += __shfl_xor(t, o, 64);
-      if (lane == 0 && u < group) red[wave][u] = t;
+    for (int q = 0; q < 4; ++q) {
+      x[q] = score_scale * acc[i][q];
+      if (4 * tc + q < n_valid) m = fmax(m, x[q]);
     }
-    __syncthreads();
-    if (threadIdx.x < group) {
-      const int u = threadIdx.x;
-      const float s = (red[0][u] + red[1][u]) + (red[2][u] + red[3][u]);
-      head_stats[((int64_t)j * num_q_heads + g * group + u) * n_chunks + chunk] = make_float2(m[u], s);
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) m = fmax(m, __shfl_xor(m, o, 64));
+    double e[4], sum = 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      e[q] = 4 * tc + q < n_valid ? exp(x[q] - m) : 0.0;
+      sum += e[q];
     }
-    __syncthreads();
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, 64);
+    if (n_valid <= 0) continue;
+    const int64_t row = (int64_t)j * num_q_heads + g * G + r % G;
+    double* w = weights + row * cand_stride + c0 + 4 * tc;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (4 * tc + q < n_valid) w[q] = e[q];
+    if (tc == 0) stats[row * n_chunks + ct] = make_double2(m, sum);
   }
 }
 
@@ -212,10 +260,12 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
 
 // grid: output row = cluster, or (cluster, KV head) with one set per KV head (row j * Hkv + g,
 // voted by the query heads of g only).
-//  1. soft-voting: each head's softmax maximum and normaliser over all candidates, combined from
-//     the chunk partials in chunk order; then per candidate the sum over heads, in head order.
-//     Token mode (kTok): the per-KV-head partial sums of the token scoring kernel are added in
-//     KV-head order instead.
+//  1. soft-voting, in fp64: wave w takes heads w, w + 16, ...; each head's softmax maximum M and
+//     normaliser S over all candidates come from the chunk partials (m_k, s_k) with a fixed lane
+//     butterfly, and each chunk gets the factor exp(m_k - M) / S (written to the factor scratch);
+//     then per candidate the sum over heads, in head order, of its weight exp(x - m_k) times the
+//     factor of its chunk, rounded once to fp32. Token mode (kTok): the per-KV-head partial sums of
+//     the token scoring kernel are added in KV-head order instead.
 //  2. threshold: the sel_cnt-th largest score, by radix selection on the score bits (scores are
 //     >= 0, so their bit patterns order like their values and the sign bit is 0) in three passes
 //     over bits 30-19, 18-7 and 6-0; wide first digits spread the scores of a cluster, which share
@@ -224,8 +274,9 @@ __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
 //  3. selected = score above the threshold, or equal to it and among the first ties in index
 //     order; written in ascending index order by an ordered compaction.
 struct VoteArgs {
-  const float* logits;         // block mode: [cluster][Hq][cand_stride]
-  const float2* head_stats;    // block mode: [cluster][Hq][n_chunks]
+  const double* weights;       // block mode: [cluster][Hq][cand_stride], exp(x - chunk max)
+  const double2* stats;        // block mode: [cluster][Hq][n_chunks], (chunk max, chunk sum)
+  double* factors;             // block mode: [cluster][Hq][n_chunks] scratch
   const float* partial;        // token mode: [cluster][Hkv][cand_stride]
   const ClusterGeo* geo;
   int n_chunks, num_q_heads, num_kv_heads, top_k;
@@ -244,7 +295,6 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   __shared__ int red_i[kVoteWaves];
   __shared__ unsigned hist[kHistBins];
   __shared__ int pick[2];
-  extern __shared__ float head_lds[];               // [Hq] maxima, then [Hq] 1 / normaliser
   const int row = blockIdx.x;
   const int sets = a.per_kv ? a.num_kv_heads : 1;
   const int j = row / sets;
@@ -265,31 +315,43 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
     const int h0 = a.per_kv ? (row % sets) * group : 0;
     const int h1 = a.per_kv ? h0 + group : num_q_heads;
     const int64_t cand_stride = a.cand_stride;
-    const float* x = a.logits + (int64_t)j * num_q_heads * cand_stride;
+    const int n_chunks = a.n_chunks;
     const int used = (n + kCandChunk - 1) / kCandChunk;
-    for (int h = h0 + (int)threadIdx.x; h < h1; h += kVoteThreads) {
-      const float2* st = a.head_stats + ((int64_t)j * num_q_heads + h) * a.n_chunks;
-      float m = -FLT_MAX;
-      for (int k = 0; k < used; ++k) m = fmaxf(m, st[k].x);
-      float s = 0.f;
-      for (int k = 0; k < used; ++k) s += st[k].y * expf(st[k].x - m);
-      head_lds[h] = m;
-      head_lds[num_q_heads + h] = 1.0f / s;
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    for (int h = h0 + wave; h < h1; h += kVoteWaves) {
+      const int64_t hrow = (int64_t)j * num_q_heads + h;
+      const double2* st = a.stats + hrow * n_chunks;
+      double m = -DBL_MAX;
+      for (int k = lane; k < used; k += 64) m = fmax(m, st[k].x);
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) m = fmax(m, __shfl_xor(m, o, 64));
+      double sum = 0.0;
+      for (int k = lane; k < used; k += 64) sum += st[k].y * exp(st[k].x - m);
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
+      const double inv = 1.0 / sum;
+      double* f = a.factors + hrow * n_chunks;
+      for (int k = lane; k < used; k += 64) f[k] = exp(st[k].x - m) * inv;
     }
-    __syncthreads();
+    __syncthreads();                                 // the factors are read by every thread below
+    const double* wts = a.weights + (int64_t)j * num_q_heads * cand_stride;
+    const double* fac = a.factors + (int64_t)j * num_q_heads * n_chunks;
     for (int c = threadIdx.x; c < n; c += kVoteThreads) {
-      float acc = 0.f;
+      const int k = c / kCandChunk;
+      double acc = 0.0;
       int h = h0;
-      for (; h + 16 <= h1; h += 16) {
-        float xv[16];
+      for (; h + 8 <= h1; h += 8) {
+        double wv[8], fv[8];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) xv[u] = x[(int64_t)(h + u) * cand_stride + c];
+        for (int u = 0; u < 8; ++u) {
+          wv[u] = wts[(int64_t)(h + u) * cand_stride + c];
+          fv[u] = fac[(int64_t)(h + u) * n_chunks + k];
+        }
 #pragma unroll
-        for (int u = 0; u < 16; ++u) acc += expf(xv[u] - head_lds[h + u]) * head_lds[num_q_heads + h + u];
+        for (int u = 0; u < 8; ++u) acc = fma(wv[u], fv[u], acc);
       }
-      for (; h < h1; ++h)
-        acc += expf(x[(int64_t)h * cand_stride + c] - head_lds[h]) * head_lds[num_q_heads + h];
-      score[c] = acc;
+      for (; h < h1; ++h) acc = fma(wts[(int64_t)h * cand_stride + c], fac[(int64_t)h * n_chunks + k], acc);
+      score[c] = (float)acc;
     }
   }
   __syncthreads();
@@ -446,46 +508,49 @@ __global__ __launch_bounds__(kThreads) void token_sum_kernel(const float* __rest
 }
 
 struct LogitsArgs {
-  const float *fingerprints, *k_rep;
+  const double* fingerprints;
+  const float* k_rep;
   const ClusterGeo* geo;
-  int parts, n_chunks, cand_stride, sink_blk, num_q_heads, num_kv_heads;
-  float score_scale;
-  float* logits;
-  float2* head_stats;
+  int n_clusters, row_tiles, n_chunks;
+  int64_t cand_stride;
+  int sink_blk, num_q_heads, num_kv_heads;
+  double score_scale;
+  double* weights;
+  double2* stats;
 };
 
 template <int D, bool kBounds>
 void launch_logits(dim3 grid, const LogitsArgs& a, hipStream_t stream) {
-  block_logits_kernel<D, kBounds><<<grid, kThreads, 0, stream>>>(a.fingerprints, a.k_rep, a.geo, a.parts, a.n_chunks,
-                                                                a.cand_stride, a.sink_blk, a.num_q_heads,
-                                                                a.num_kv_heads, a.score_scale, a.logits, a.head_stats);
+  block_logits_kernel<D, kBounds><<<grid, kThreads, 0, stream>>>(
+      a.fingerprints, a.k_rep, a.geo, a.n_clusters, a.row_tiles, a.n_chunks, a.cand_stride, a.sink_blk,
+      a.num_q_heads, a.num_kv_heads, a.score_scale, a.weights, a.stats);
 }
 
 }  // namespace
 
 hipError_t launch_fingerprints(const uint16_t* q, const ClusterGeo* geo, int n_clusters,
-                               int num_q_heads, int head_dim, float* fingerprints, hipStream_t stream) {
+                               int num_q_heads, int head_dim, float* fingerprints, double* fingerprints64,
+                               hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
   const int row_elems = num_q_heads * head_dim;
   const dim3 grid((row_elems + kFpCols - 1) / kFpCols, n_clusters);
-  fingerprint_kernel<<<grid, kFpThreads, 0, stream>>>(q, geo, row_elems, fingerprints);
+  fingerprint_kernel<<<grid, kFpThreads, 0, stream>>>(q, geo, row_elems, fingerprints, fingerprints64);
   return hipGetLastError();
 }
 
 int selection_chunks(int max_cand) { return (max_cand + kCandChunk - 1) / kCandChunk; }
 
-hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, const ClusterGeo* geo,
-                               int n_clusters, int max_cand, int cand_stride, int sink_blk,
-                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, float score_scale,
-                               float* logits, float2* head_stats, hipStream_t stream) {
+hipError_t launch_block_logits(const double* fingerprints, const float* k_rep, const ClusterGeo* geo,
+                               int n_clusters, int max_cand, int64_t cand_stride, int sink_blk,
+                               int num_q_heads, int num_kv_heads, int head_dim, bool bounds, double score_scale,
+                               double* weights, double2* stats, hipStream_t stream) {
   if (n_clusters <= 0 || max_cand <= 0) return hipSuccess;
   const int n_chunks = selection_chunks(max_cand);
-  // enough work-groups to fill the chip, without launching many that find no chunk
-  const int64_t base = (int64_t)n_clusters * num_kv_heads;
-  const int parts = (int)std::min<int64_t>(n_chunks, std::max<int64_t>(1, (kLogitsTargetGroups + base - 1) / base));
-  const dim3 grid((unsigned)(base * parts));
-  const LogitsArgs a{fingerprints, k_rep, geo, parts, n_chunks, cand_stride, sink_blk, num_q_heads, num_kv_heads,
-                     score_scale, logits, head_stats};
+  const int64_t rows = (int64_t)n_clusters * (num_q_heads / num_kv_heads);
+  const int row_tiles = (int)((rows + kLgRows - 1) / kLgRows);
+  const dim3 grid((unsigned)((int64_t)n_chunks * row_tiles * num_kv_heads));
+  const LogitsArgs a{fingerprints, k_rep, geo, n_clusters, row_tiles, n_chunks, cand_stride, sink_blk,
+                     num_q_heads, num_kv_heads, score_scale, weights, stats};
   if (head_dim == 128)
     bounds ? launch_logits<128, true>(grid, a, stream) : launch_logits<128, false>(grid, a, stream);
   else
@@ -493,14 +558,15 @@ hipError_t launch_block_logits(const float* fingerprints, const float* k_rep, co
   return hipGetLastError();
 }
 
-hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const ClusterGeo* geo, int n_clusters,
-                            int max_cand, int cand_stride, int sink_blk, int num_q_heads, int num_kv_heads,
-                            bool per_kv, int top_k, int n_blocks, float* spill, int32_t* sel_idx, int32_t* sel_cnt,
-                            float* scores_out, hipStream_t stream) {
+hipError_t launch_vote_topk(const double* weights, const double2* stats, double* factors, const ClusterGeo* geo,
+                            int n_clusters, int max_cand, int64_t cand_stride, int sink_blk, int num_q_heads,
+                            int num_kv_heads, bool per_kv, int top_k, int n_blocks, float* spill, int32_t* sel_idx,
+                            int32_t* sel_cnt, float* scores_out, hipStream_t stream) {
   if (n_clusters <= 0) return hipSuccess;
   VoteArgs a{};
-  a.logits = logits;
-  a.head_stats = head_stats;
+  a.weights = weights;
+  a.stats = stats;
+  a.factors = factors;
   a.geo = geo;
   a.n_chunks = selection_chunks(max_cand);
   a.num_q_heads = num_q_heads;
@@ -514,8 +580,7 @@ hipError_t launch_vote_topk(const float* logits, const float2* head_stats, const
   a.sel_idx = sel_idx;
   a.sel_cnt = sel_cnt;
   a.scores_out = scores_out;
-  const size_t lds = sizeof(float) * 2 * (size_t)num_q_heads;
-  vote_topk_kernel<false><<<n_clusters * (per_kv ? num_kv_heads : 1), kVoteThreads, lds, stream>>>(a);
+  vote_topk_kernel<false><<<n_clusters * (per_kv ? num_kv_heads : 1), kVoteThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -45,10 +45,11 @@ def run_layer(h: Scale, q, k_pages, v_pages, block_table, n_tokens: int, cluster
     """Enqueue the whole hot path of one layer on the handle's stream (no synchronisation)."""
     cs = np.asarray(cluster_start, dtype=np.int32)
     if h.cfg.select_tokens:
-        h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores,
-                                bufs.fingerprints)
+        h.select_cluster_tokens(q, n_tokens, k_pages, block_table, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores)
     else:
         h.rep_keys(k_pages, block_table, n_tokens, bufs.k_rep)
-        h.select_cluster(q, n_tokens, bufs.k_rep, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores, bufs.fingerprints)
+        h.select_cluster(q, n_tokens, bufs.k_rep, cs, bufs.sel_idx, bufs.sel_cnt, bufs.scores)
+    if bufs.fingerprints is not None:
+        h.fingerprints(bufs.fingerprints, len(cs) - 1)
     h.sparse_prefill(q, k_pages, v_pages, block_table, n_tokens, cs, bufs.sel_idx, bufs.sel_cnt, bufs.out)
     return bufs

@@ -45,21 +45,24 @@ def config(w: gen.Workload, n_clusters: int, out_bf16=False, **over):
     return pk.config_for(out_bf16=out_bf16, **kw)
 
 
+def upload(data: dict, dev, n_tokens=None):
+    """Device copies (q, k_pages, v_pages, block_table) of a generated layer."""
+    q = data["q"] if n_tokens is None else data["q"][:n_tokens]
+    return to_dev(q, dev), to_dev(data["k_pages"], dev), to_dev(data["v_pages"], dev), to_dev(data["block_table"], dev)
+
+
 def run_gpu(w: gen.Workload, data: dict, cs, dev, *, out_bf16=False, n_tokens=None, with_scores=True, out_rows=None,
-            **over):
+            dev_data=None, **over):
     """Whole path on the GPU; returns host copies of every output plus the call counter.
     With `out_rows`, only those rows of the attention output are copied back (res["out"][i] is
-    row out_rows[i])."""
+    row out_rows[i]). `dev_data` gives inputs already on the device (as `upload` returns them)."""
     import torch
 
     import paper_2609_31568_amd as pk
 
     n = w.n_tokens if n_tokens is None else n_tokens
     cfg = config(w, len(cs) - 1, out_bf16=out_bf16, **over)
-    q = to_dev(data["q"][:n], dev)
-    kp = to_dev(data["k_pages"], dev)
-    vp = to_dev(data["v_pages"], dev)
-    bt = to_dev(data["block_table"], dev)
+    q, kp, vp, bt = dev_data if dev_data is not None else upload(data, dev, n)
     with pk.Scale(cfg) as h:
         bufs = pk.LayerBuffers(cfg, n, len(cs) - 1, device=dev, with_scores=with_scores)
         pk.run_layer(h, q, kp, vp, bt, n, cs, bufs)
@@ -91,54 +94,24 @@ def check_rounding(gpu: np.ndarray, ref: np.ndarray, what: str):
 
 U32 = 2.0 ** -24
 
-
-def score_bounds(ref, num_kv_heads: int, score_scale: float = 1.0, k_bounds=None):
-    """First-order error bound of the GPU's fp32 soft-voting scores, per cluster and candidate.
-
-    GPU logits are fp32 dot products of the fp32-rounded fingerprint and representative key:
-    |dx| <= (d + 2) u sum_i |v_i k_i| =: dX (recursive-summation bound plus the two input
-    roundings). A softmax weight p moves by at most 2 p dX under logit perturbations of at most
-    dX; the exponent's argument x - max carries a rounding of u |x - max|; exp, the normaliser
-    (n_cand terms) and the sum over heads add (n_cand + Hq + 8) u relative. Hence
-    |d score_b| <= score_b (2 dX + 2 u R + (n_cand + Hq + 8) u) + 1e-9, with R the logit range.
-    With the channel-wise bounds ``k_bounds`` = (mn, mx), the logit's terms are max(v_i mn_i,
-    v_i mx_i), each within u of its value, so sum_i |v_i k_i| becomes sum_i max(|v_i mn_i|, |v_i mx_i|).
-    """
-    out = []
-    for g, v, sc in zip(ref["geometry"], ref["fingerprints"], ref["scores"]):
-        if g.n_cand == 0:
-            out.append(np.zeros(0))
-            continue
-        Hq, d = v.shape
-        heads_g = (np.arange(Hq) * num_kv_heads) // Hq
-        c = slice(g.sink_blk, g.sink_blk + g.n_cand)
-        if k_bounds is None:
-            kr = ref["k_rep"][c]                                    # [n, Hkv, d]
-            absdot = np.einsum("hi,nhi->hn", np.abs(v), np.abs(kr[:, heads_g, :])) * abs(score_scale)
-            x = np.einsum("hi,nhi->hn", v, kr[:, heads_g, :]) * score_scale
-        else:
-            mn, mx = k_bounds[0][c][:, heads_g, :], k_bounds[1][c][:, heads_g, :]     # [n, Hq, d]
-            absdot = np.maximum(np.abs(v[None] * mn), np.abs(v[None] * mx)).sum(axis=2).T * abs(score_scale)
-            x = np.maximum(v[None] * mn, v[None] * mx).sum(axis=2).T * score_scale
-        dX = (d + 2) * U32 * absdot.max()
-        R = float((x.max(axis=1) - x.min(axis=1)).max())
-        rel = 2 * dX + 2 * U32 * R + (g.n_cand + Hq + 8) * U32
-        out.append(sc * rel + 1e-9)
-    return out
+# Block-level soft-voting scores: fp64 arithmetic on the GPU, each score rounded once to fp32 (at
+# most 9.5e-7 for a score below Hq = 32, far less for the scores of about 0.01-5 seen here); the
+# acceptance is a fixed absolute tolerance.
+SCORE_ATOL = 1e-6
 
 
-def check_scores(gpu_scores: np.ndarray, ref, num_kv_heads: int, what: str, score_scale: float = 1.0, k_bounds=None):
-    """Candidates within the bound above; every other entry of the row is -1."""
+def check_scores(gpu_scores: np.ndarray, ref, what: str):
+    """Candidates within SCORE_ATOL of the fp64 oracle; every other entry of the row is -1.
+    Returns the largest error seen."""
     worst = 0.0
     nb = gpu_scores.shape[1]
-    bounds = score_bounds(ref, num_kv_heads, score_scale, k_bounds)
-    for j, (g, sc, bound) in enumerate(zip(ref["geometry"], ref["scores"], bounds)):
+    for j, (g, sc) in enumerate(zip(ref["geometry"], ref["scores"])):
         row = gpu_scores[j]
         cand = np.arange(g.sink_blk, g.sink_blk + g.n_cand)
         assert np.all(np.delete(row, cand) == -1.0), f"{what} cluster {j}: non-candidate entry is not -1"
         if g.n_cand:
             err = np.abs(row[cand].astype(np.float64) - sc)
-            assert np.all(err <= bound), f"{what} cluster {j}: score error {err.max():.2e} above bound"
+            assert np.all(err <= SCORE_ATOL), f"{what} cluster {j}: score error {err.max():.2e} above {SCORE_ATOL}"
             worst = max(worst, float(err.max()))
         assert nb >= g.sink_blk + g.n_cand
     return worst
@@ -186,8 +159,9 @@ def token_score_bounds(ref, cands, num_kv_heads: int, score_scale: float = 1.0):
     return out
 
 
-def check_token_scores(gpu_scores: np.ndarray, ref, bounds, block_size: int, what: str):
-    """Candidate entries within the bound; every other entry of the row is -1."""
+def check_token_scores(gpu_scores: np.ndarray, ref, bounds, block_size: int, what: str, atol=None):
+    """Candidate entries within the bound (and within `atol` when given); every other entry of the
+    row is -1. Returns the largest relative error seen."""
     worst = 0.0
     for j, (g, sc, bd) in enumerate(zip(ref["geometry"], ref["scores"], bounds)):
         row = gpu_scores[j]
@@ -197,6 +171,8 @@ def check_token_scores(gpu_scores: np.ndarray, ref, bounds, block_size: int, wha
         if g.n_cand:
             err = np.abs(row[first:first + g.n_cand].astype(np.float64) - sc)
             assert np.all(err <= bd), f"{what} cluster {j}: score error {err.max():.2e} above bound"
+            if atol is not None:
+                assert np.all(err <= atol), f"{what} cluster {j}: score error {err.max():.2e} above {atol}"
             worst = max(worst, float((err / np.maximum(sc, 1e-300)).max()))
     return worst
 
@@ -238,8 +214,15 @@ def check_token_selection(gpu_sel, gpu_cnt, gpu_scores, ref, bounds, block_size:
     return n_exact
 
 
-def check_selection(gpu_sel, gpu_cnt, ref, eps: float):
-    """Exact where the oracle's margin exceeds MARGIN; eps-valid top-k everywhere."""
+# With every score within SCORE_ATOL of the oracle's, a top-k margin above twice that leaves the GPU
+# no other set to select: the k-th and (k+1)-th scores cannot swap.
+MARGIN_EXACT = 2 * SCORE_ATOL
+
+
+def check_selection(gpu_sel, gpu_cnt, ref, eps: float, margin_exact: float = MARGIN_EXACT):
+    """Exact where the oracle's margin exceeds `margin_exact` (the scores' tolerance makes the set
+    unique there; it is far below the 1e-3 of the acceptance rule); eps-valid top-k everywhere.
+    Returns the number of clusters whose margin exceeds MARGIN (1e-3), all of them exact."""
     n_exact = 0
     for j, (g, s_ref, m, sc) in enumerate(zip(ref["geometry"], ref["selections"], ref["margins"], ref["scores"])):
         cnt = int(gpu_cnt[j])
@@ -248,9 +231,9 @@ def check_selection(gpu_sel, gpu_cnt, ref, eps: float):
         assert np.all(gpu_sel[j, cnt:] == -1), f"cluster {j}: padding is not -1"
         assert np.all(np.diff(got) > 0), f"cluster {j}: not strictly ascending"
         assert np.all((got >= g.sink_blk) & (got < g.sink_blk + g.n_cand)), f"cluster {j}: non-candidate selected"
-        if m > MARGIN:
+        if m > min(MARGIN, margin_exact):
             assert np.array_equal(got, s_ref), f"cluster {j}: {got} != oracle {s_ref} (margin {m:.2e})"
-            n_exact += 1
+            n_exact += m > MARGIN
         if 0 < cnt < g.n_cand:
             kth = np.sort(sc)[::-1][cnt - 1]
             chosen = np.zeros(g.n_cand, dtype=bool)

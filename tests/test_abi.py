@@ -81,11 +81,16 @@ def test_init_rejects_bad_config_before_any_hip_call(over, status):
     for k, v in raw.items():
         setattr(cfg, k, v)                  # the raw field, past make_config's conversions
     h = ctypes.c_void_p(1234)
-    st = pk.lib.scale_init(ctypes.byref(cfg), None, ctypes.byref(h))
+    st = pk.lib.scale_init_variant(ctypes.byref(cfg.base), ctypes.byref(cfg.variant), None, ctypes.byref(h))
     assert st == status
     assert h.value is None
+    if not raw:                             # the default path through scale_init rejects it the same way
+        h = ctypes.c_void_p(1234)
+        assert pk.lib.scale_init(ctypes.byref(cfg.base), None, ctypes.byref(h)) == status
+        assert h.value is None
     assert pk.lib.scale_init(None, None, ctypes.byref(h)) == -1
-    assert pk.lib.scale_init(ctypes.byref(_cfg()), None, None) == -1
+    assert pk.lib.scale_init(ctypes.byref(_cfg().base), None, None) == -1
+    assert pk.lib.scale_init_variant(None, None, None, ctypes.byref(h)) == -1
 
 
 def test_calls_reject_null_handle():
@@ -93,7 +98,7 @@ def test_calls_reject_null_handle():
     lib = pk.lib
     cs = np.array([0, 1], dtype=np.int32)
     assert lib.scale_rep_keys(None, 1, None, 128, 1) == -1
-    assert lib.scale_select_cluster(None, 1, 128, 1, cs.ctypes.data, 1, 1, 1, None, None) == -1
+    assert lib.scale_select_cluster(None, 1, 128, 1, cs.ctypes.data, 1, 1, 1, None) == -1
     assert lib.scale_sparse_prefill(None, 1, 1, 1, None, 128, cs.ctypes.data, 1, 1, 1, 1) == -1
     n = ctypes.c_int64()
     assert lib.scale_retrieval_calls(None, ctypes.byref(n)) == -1
@@ -101,7 +106,8 @@ def test_calls_reject_null_handle():
     k = ctypes.c_int32()
     assert lib.scale_cluster_subchunks(None, 1, 128, 0, 0.95, 4096, 0, out.ctypes.data, ctypes.byref(k), None) == -1
     assert lib.scale_rep_keys_range(None, 1, None, 0, 128, 1) == -1
-    assert lib.scale_select_cluster_tokens(None, 1, 128, 1, None, cs.ctypes.data, 1, 1, 1, None, None) == -1
+    assert lib.scale_select_cluster_tokens(None, 1, 128, 1, None, cs.ctypes.data, 1, 1, 1, None) == -1
+    assert lib.scale_fingerprints(None, 1, 1) == -1
     lib.scale_free(None)        # no-op
 
 
@@ -184,7 +190,8 @@ def test_geometry_rejects_malformed_clusters(cs, n, status):
                sink_tokens=64, local_window=256, max_tokens=8192, max_clusters=8)
     arr = np.asarray(cs, dtype=np.int32)
     geo = np.zeros((len(cs), 6), dtype=np.int32)
-    st = pk.lib.scale_cluster_geometry(ctypes.byref(cfg), n, arr.ctypes.data, len(cs) - 1, geo.ctypes.data)
+    st = pk.lib.scale_cluster_geometry(ctypes.byref(cfg.base), None, n, arr.ctypes.data, len(cs) - 1,
+                                       geo.ctypes.data)
     assert st == status
 
 
@@ -194,9 +201,9 @@ def test_geometry_capacity():
                sink_tokens=64, local_window=256, max_tokens=2048, max_clusters=2)
     geo = np.zeros((8, 6), dtype=np.int32)
     cs = gen.cluster_starts(8, 1)
-    assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg), 2048, cs.ctypes.data, 8, geo.ctypes.data) == -4
+    assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg.base), None, 2048, cs.ctypes.data, 8, geo.ctypes.data) == -4
     cs = gen.cluster_starts(16, 8)
-    assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg), 4096, cs.ctypes.data, 2, geo.ctypes.data) == -4
+    assert pk.lib.scale_cluster_geometry(ctypes.byref(cfg.base), None, 4096, cs.ctypes.data, 2, geo.ctypes.data) == -4
 
 
 def test_c_client_of_the_header(tmp_path):
@@ -217,4 +224,4 @@ def test_c_client_of_the_header(tmp_path):
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
     assert run.returncode == 0, run.stdout + run.stderr
-    assert run.stdout.count("ok ") == 4
+    assert run.stdout.count("ok ") == 5

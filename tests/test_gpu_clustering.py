@@ -144,7 +144,7 @@ def test_path_driven_by_gpu_clusters(dev):
     ref = oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, sub_chunk=w.sub_chunk,
                          block_size=w.block_size, top_k=w.top_k, sink_tokens=w.sink_tokens,
                          local_window=w.local_window, cluster_start=cs, with_output=False)
-    gu.check_scores(res["scores"], ref, w.num_kv_heads, "scr128k")
+    gu.check_scores(res["scores"], ref, "scr128k")
     gu.check_selection(res["sel_idx"], res["sel_cnt"], ref, 1e-5)
     rows = gu.sample_rows(ref["geometry"], np.random.default_rng(12), tiles_per_cluster=0)
     sels = gu.gpu_selections(res, len(cs) - 1)
@@ -226,18 +226,27 @@ def test_topk_overlap_matches_oracle(dev):
     rc = oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, cluster_start=cs, **kw)
     r1 = oracle.prefill(d["q"], d["k_pages"], d["v_pages"], d["block_table"], w.n_tokens, cluster_start=one, **kw)
     rho_ref = oracle.topk_overlap(rc["selections"], r1["selections"], cs)
-    # where every selection involved clears the margin the sets are unique and rho must match
-    # exactly; elsewhere near-ties may swap a few equally valid blocks (eps-valid sets)
+    # every selection involved, the clusters' and the single sub-chunks', is exact above the margin
+    # and eps-valid everywhere
+    gu.check_selection(np.stack([np.pad(s, (0, w.top_k - len(s)), constant_values=-1) for s in sel_c]),
+                       np.array([len(s) for s in sel_c]), rc, 1e-5)
+    gu.check_selection(np.stack([np.pad(s, (0, w.top_k - len(s)), constant_values=-1) for s in sel_1]),
+                       np.array([len(s) for s in sel_1]), r1, 1e-5)
+    # rho is a host function of the sets: where the GPU's sets of a cluster and of all its members
+    # equal the oracle's, it must be equal; elsewhere near-ties may swap a few equally valid blocks.
+    # With fp64 scores the sets differ only at near-exact ties, so at least half the clusters are
+    # compared exactly.
     checked = 0
     for j in range(k):
-        margins = [rc["margins"][j]] + [r1["margins"][i] for i in range(cs[j], cs[j + 1])]
+        same = np.array_equal(sel_c[j], rc["selections"][j]) and all(
+            np.array_equal(sel_1[i], r1["selections"][i]) for i in range(cs[j], cs[j + 1]))
         both_nan = math.isnan(rho_gpu[j]) and math.isnan(rho_ref[j])
-        if min(margins) > gu.MARGIN:
+        if same:
             assert both_nan or rho_gpu[j] == rho_ref[j], j
             checked += 1
         else:
             assert both_nan or abs(rho_gpu[j] - rho_ref[j]) <= 0.1, j
-    assert checked >= 1
+    assert checked >= k // 2, (checked, k)
     finite = rho_gpu[~np.isnan(rho_gpu)]
     gu.log(f"[clustering] llama32k-scr rho over {len(finite)} clusters: min {finite.min():.3f} median "
            f"{np.median(finite):.3f} mean {finite.mean():.3f} ({checked} checked against the oracle)")
