@@ -184,6 +184,23 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
                                   int32_t n_clusters, int32_t* sel_idx, int32_t* sel_cnt,
                                   float* scores_out);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops or
+ * harnesses that forbid hipMalloc): scale_select_cluster on the default path (block level, mean
+ * representative keys, one set per cluster) with no handle. The call allocates nothing: its
+ * scratch is one 64 MiB device array of the library, which every device it runs on holds for the
+ * life of the process, and the cluster geometry is computed on the device from cluster_start
+ * passed by value. Arguments, validation, results and errors as for scale_init (cfg) and
+ * scale_select_cluster, with `hip_stream` the stream to enqueue on (NULL: the default stream).
+ * A call whose scratch would exceed the array (about n_clusters * Hq * (n_tokens / B) * 8 bytes
+ * for the per-candidate weights, plus fingerprints and statistics; the 128K Llama-3-8B layer in
+ * clusters of 8 needs about 10 MiB) returns SCALE_ERR_CAPACITY before any device work. Calls on
+ * one device share the array: calls that overlap in time on one device race, so serialise them
+ * (one stream, or events). No retrieval-call counter is kept (there is no handle). */
+scale_status scale_select_cluster_static(const scale_config* cfg, void* hip_stream, const uint16_t* q,
+                                         int32_t n_tokens, const float* k_rep, const int32_t* cluster_start,
+                                         int32_t n_clusters, int32_t* sel_idx, int32_t* sel_cnt,
+                                         float* scores_out);
+
 /* Token-level cluster selection (Eq. 9 with head soft-voting, Sec. 5.1.3, at the granularity of
  * single tokens); handles created with select_tokens = 1 only (else SCALE_ERR_UNSUPPORTED):
  *   v[h]     = mean of q[p][h] over the anchor rows

@@ -29,7 +29,7 @@ EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
     "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range", "scale_select_cluster_tokens",
-    "scale_init_variant", "scale_fingerprints",
+    "scale_init_variant", "scale_fingerprints", "scale_select_cluster_static",
 )
 STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster", "gather")
 
@@ -102,6 +102,8 @@ def _load():
     lib.scale_select_cluster_tokens.restype = ctypes.c_int
     lib.scale_fingerprints.argtypes = [vp, vp, i32]
     lib.scale_fingerprints.restype = ctypes.c_int
+    lib.scale_select_cluster_static.argtypes = [ctypes.POINTER(scale_config), vp, vp, i32, vp, vp, i32, vp, vp, vp]
+    lib.scale_select_cluster_static.restype = ctypes.c_int
     lib.scale_sparse_prefill.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, vp, vp, vp]
     lib.scale_sparse_prefill.restype = ctypes.c_int
     lib.scale_status_string.argtypes = [ctypes.c_int]
@@ -301,6 +303,19 @@ def scale_select_cluster_tokens(h: Scale, q, n_tokens, k_pages, block_table, clu
 
 def scale_fingerprints(h: Scale, out, n_clusters):
     h.fingerprints(out, n_clusters)
+
+
+def scale_select_cluster_static(cfg: Config, q, n_tokens, k_rep, cluster_start, sel_idx, sel_cnt, scores_out=None,
+                                stream=None):
+    """The allocation-free selection (no handle; the library's static device scratch)."""
+    cs = _cluster_start(cluster_start)
+    _check(lib.scale_select_cluster_static(ctypes.byref(cfg.base), _stream_handle(stream), _ptr(q), int(n_tokens),
+                                           _ptr(k_rep), cs.ctypes.data, len(cs) - 1, _ptr(sel_idx), _ptr(sel_cnt),
+                                           _ptr(scores_out)), "scale_select_cluster_static")
+
+
+def scale_sparse_prefill(h: Scale, q, k_pages, v_pages, block_table, n_tokens, cluster_start, sel_idx, sel_cnt, out):
+    h.sparse_prefill(q, k_pages, v_pages, block_table, n_tokens, cluster_start, sel_idx, sel_cnt, out)
 
 
 def scale_retrieval_calls(h: Scale) -> int:
