@@ -29,10 +29,11 @@
 // h hold the 16 consecutive keys [16h, 16h + 16) of each 32-key block; a 16-key PV step then takes
 // 8 consecutive keys from each lane half, which the V^T operand reads as one 16-byte chunk.
 //
-// Order inside a tile: S(keys 0-31), S(keys 32-63), softmax(0-31), PV(0-31), softmax(32-63),
-// PV(32-63). Each group of eight MFMAs has its eight LDS operand reads issued ahead of it. MFMAs
-// run asynchronously, so each half's VALU softmax overlaps the MFMAs issued just before it
-// within the wave; the second wave on the SIMD fills what is left.
+// Order inside a tile: S(keys 0-31); S(keys 32-63) interleaved with the softmax of keys 0-31;
+// PV(0-31) interleaved with the softmax of keys 32-63; PV(32-63) with the stores of the next tile
+// into LDS. Each softmax shares a scheduling region with the MFMAs it overlaps (LLVM's
+// MFMA / exponential interleave strategy places them), and the stores are unconditional (past the
+// last tile they write the idle buffer), so no branch separates them from the last MFMAs.
 //
 // Pipelining: LDS holds two tile buffers, and two register sets stage the global loads. A tile's
 // loads are issued two tiles ahead; they are written to LDS at the end of the tile before it, and
@@ -163,8 +164,8 @@ __device__ __forceinline__ void store_tile(const u32x4 (&kreg)[S::kPer], const u
       uint32_t* dst = vt + (8 * c) * S::kVtStrideDw + 4 * (c & 7) + kp;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        dst[(2 * e) * S::kVtStrideDw] = (a[e] & 0xFFFFu) | (b[e] << 16);
-        dst[(2 * e + 1) * S::kVtStrideDw] = (a[e] >> 16) | (b[e] & 0xFFFF0000u);
+        dst[(2 * e) * S::kVtStrideDw] = __builtin_amdgcn_perm(b[e], a[e], 0x05040100u);   // low halves
+        dst[(2 * e + 1) * S::kVtStrideDw] = __builtin_amdgcn_perm(b[e], a[e], 0x07060302u); // high halves
       }
     }
   }
@@ -306,57 +307,41 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
     const uint16_t* k_lds = lds + buf * S::kBufElems;
     const uint16_t* v_lds = k_lds + S::kKElems;
 
-    // S^T for the two 32-key halves of the tile.
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    // S^T of half 0, then S^T of half 1 interleaved with the softmax of half 0, then PV of half 0
+    // interleaved with the softmax of half 1, then PV of half 1.
+    auto s_half = [&](int kb, f32x16& acc) {
       const uint16_t* krow = k_lds + k_off + 32 * kb * S::kKStride;
       bf16x8 kf[D / 16];
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) kf[c] = *reinterpret_cast<const bf16x8*>(krow + 16 * c);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[0], f32x16{}, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[0], f32x16{}, 0, 0, 0);
 #pragma unroll
-      for (int c = 1; c < D / 16; ++c) s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c], qf[c], s[kb], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, D / 16, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, D / 16, 0);
-    }
-
-    // Padding rows of a partial last gathered tile (keys sel_rem .. 63) take no weight.
-    if constexpr (TOK) {
-      if (sel_rem != 0 && t == n_fixed - 1) {
-        const int lim = sel_rem - 16 * half;     // accumulator e of block kb is key 32kb + 16half + e
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int c = 1; c < D / 16; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c], qf[c], acc, 0, 0, 0);
+    };
+    auto mask_half = [&](int kb, f32x16& sc) {
+      if constexpr (TOK) {
+        if (sel_rem != 0 && t == n_fixed - 1) {
+          const int lim = sel_rem - 16 * half;
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (32 * kb + e >= lim) s[kb][e] = -INFINITY;
+            if (32 * kb + e >= lim) sc[e] = -INFINITY;
+        }
       }
-    }
-    // Causal mask only on a local tile that reaches this wave's positions.
-    if (t >= n_fixed) {
-      const int key0 = local0 + (t - n_fixed) * kKeyTile;
-      if (key0 + kKeyTile > wave_p0) {
-        const int lim = p - key0 - 16 * half;    // accumulator e of block kb is key 32kb + 16half + e
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      if (t >= n_fixed) {
+        const int key0 = local0 + (t - n_fixed) * kKeyTile;
+        if (key0 + kKeyTile > wave_p0) {
+          const int lim = p - key0 - 16 * half;
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (32 * kb + e > lim) s[kb][e] = -INFINITY;
+            if (32 * kb + e > lim) sc[e] = -INFINITY;
+        }
       }
-    }
-    // Softmax and PV one 32-key half at a time. Weights are first taken against the row's
-    // reference max; their bf16 sum (v_dot2 with ones) doubles as the overflow check: a sum
-    // above 2^20 (or inf / NaN) means a score exceeded the reference by about 2^15 or more, and
-    // the half is redone exactly (true max, O and denominator rescaled). The first tile always
-    // takes that path, since the reference starts at -1e30.
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      bf16x8 pf[2];
-      float lsum = half_weights(s[kb], m_ref * qk_scale_log2, qk_scale_log2, pf);
+    };
+    auto finish = [&](const f32x16& sc, float lsum, bf16x8 (&pf)[2]) {
       if (__any(!(lsum <= kWeightSumLimit))) {
-        float mt = fmaxf(s[kb][0], s[kb][1]);
+        float mt = fmaxf(sc[0], sc[1]);
 #pragma unroll
-        for (int e = 2; e < 16; ++e) mt = fmaxf(mt, s[kb][e]);
+        for (int e = 2; e < 16; ++e) mt = fmaxf(mt, sc[e]);
         mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
         const float m_new = fmaxf(m_ref, mt);
         const float alpha = fast_exp2((m_ref - m_new) * qk_scale_log2);
@@ -366,27 +351,43 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
 #pragma unroll
           for (int e = 0; e < 16; ++e) o[db][e] *= alpha;
         m_ref = m_new;
-        lsum = half_weights(s[kb], m_ref * qk_scale_log2, qk_scale_log2, pf);
+        lsum = half_weights(sc, m_ref * qk_scale_log2, qk_scale_log2, pf);
       }
       l_run += lsum;
-
-      // O^T += V^T P^T over this half's two 16-key steps: step u takes keys 32kb + 16h + 8u + [0, 8)
-      // from lane half h, which is entries [8u, 8u + 8) of s[kb] and one 16-byte V^T chunk.
+    };
+    auto pv_half = [&](int kb, const bf16x8 (&pf)[2]) {
       bf16x8 vf[D / 32][2];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int u = 0; u < 2; ++u) vf[db][u] = *reinterpret_cast<const bf16x8*>(v_lds + vt_off[db] + 2 * (16 * kb + 4 * u));
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int u = 0; u < 2; ++u) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db][u], pf[u], o[db], 0, 0, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x100, D / 16, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, D / 16, 1);
+    };
+    f32x16 s0, s1;
+    bf16x8 pf0[2], pf1[2];
+    s_half(0, s0);
+    mask_half(0, s0);
+    {
+      s_half(1, s1);
+      const float l0 = half_weights(s0, m_ref * qk_scale_log2, qk_scale_log2, pf0);
+      __builtin_amdgcn_iglp_opt(2);   // interleave the exponentials with the MFMAs
+      finish(s0, l0, pf0);
     }
+    mask_half(1, s1);
+    {
+      pv_half(0, pf0);
+      const float l1 = half_weights(s1, m_ref * qk_scale_log2, qk_scale_log2, pf1);
+      __builtin_amdgcn_iglp_opt(2);
+      finish(s1, l1, pf1);
+    }
+    pv_half(1, pf1);
 
-    if (t + 1 < n_tiles) store_tile<S, D>(ks, vs, lds + (buf ^ 1) * S::kBufElems, tid);
+    // Past the last tile this stores the re-read last tile into the idle buffer: unconditional, so
+    // the stores share a scheduling region with the last PV MFMAs.
+    store_tile<S, D>(ks, vs, lds + (buf ^ 1) * S::kBufElems, tid);
     __syncthreads();
   };
   for (int t = 0; t < n_tiles; t += 2) {
