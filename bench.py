@@ -88,6 +88,10 @@ def parse_args(argv=None):
     ap.add_argument("--out-bf16", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy 1 GiB device to device (reference for HBM byte counters) and exit")
+    ap.add_argument("--gemm-probe", type=float, default=0.0, metavar="SECONDS",
+                    help="only run a dense 8192^3 bf16 library GEMM for SECONDS and print its TFLOP/s (the "
+                         "MFMA rate the chip sustains at its power limit, a reference for the attention "
+                         "roofline) and exit")
     return ap.parse_args(argv)
 
 
@@ -522,6 +526,23 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes_read": a.numel() * 4, "copy_probe_bytes_written": b.numel() * 4}))
+        return
+    if args.gemm_probe > 0:
+        n = 8192
+        a = torch.randn(n, n, dtype=torch.bfloat16, device=dev)
+        b = torch.randn(n, n, dtype=torch.bfloat16, device=dev)
+        for _ in range(5):
+            c = a @ b
+        torch.cuda.synchronize()
+        done, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < args.gemm_probe:
+            for _ in range(50):
+                c = a @ b
+            torch.cuda.synchronize()
+            done += 50
+        dt = time.perf_counter() - t0
+        print(json.dumps({"gemm_probe": f"{n}^3 bf16 torch.matmul", "launches": done, "seconds": round(dt, 2),
+                          "tflops": round(2 * n ** 3 * done / dt / 1e12, 1), "checksum": float(c[0, 0])}))
         return
     w = gen.WORKLOADS[args.workload]
     sweep = [int(x) for x in args.sweep.split(",")] if args.sweep else [args.cluster or w.cluster]
