@@ -97,6 +97,7 @@ def parse_args(argv=None):
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_traffic_llama128k.md")
 COUNTER_PROFILE = os.path.join(ROOT, "profiles", "attention_counters_llama128k.md")
+POWER_PROFILE = os.path.join(ROOT, "profiles", "clock_power_mi355x.md")
 ORACLE_FULL_PROFILE = os.path.join(ROOT, "profiles", "oracle_full_layer_llama128k.md")
 
 
@@ -125,6 +126,19 @@ def measured_traffic():
     copy-probe factors."""
     block = profile_block(TRAFFIC_PROFILE)
     return int(block["traffic_bytes"]) if block else None
+
+
+def library_gemm_reference(achieved):
+    """The bf16 rate a dense library GEMM sustains on this part at its power limit (committed
+    measurement, `--gemm-probe`), and the attention rate as a fraction of it: context for the
+    nominal-peak fraction, not a replacement for it."""
+    block = profile_block(POWER_PROFILE)
+    if not block:
+        return None
+    ref = float(block["library_gemm_tflops"])
+    return {"tflops": ref, "frac": round(achieved / ref, 4), "what": block["library_gemm"],
+            "clock_mhz": block["library_gemm_clock_mhz"],
+            "source": os.path.relpath(POWER_PROFILE, ROOT)}
 
 
 def counted_mfma(alg_flops, launch_ms):
@@ -442,6 +456,7 @@ def time_path(args, w, c, layers, dev, theta=None):
             "avg_launch_ms": round(att_ms, 4),
             "median_launch_ms": round(per_step[len(per_step) // 2], 4),
             "min_launch_ms": round(per_step[0], 4),
+            "library_gemm": library_gemm_reference(achieved),
         },
         "mfma_util_pct": round(100 * achieved / PEAK_BF16_TFLOPS, 2),
         "mfma_counted": counted_mfma(work["attention_flops"], att_ms) if profiled else None,
