@@ -75,3 +75,23 @@ def test_static_selection_equals_handle_selection(dev):
     with pytest.raises(pk.ScaleError) as e:
         pk.scale_select_cluster_static(cfg, 1, w.n_tokens, 1, cs, 1, 1, None)
     assert e.value.status == pk.SCALE_ERR_CAPACITY
+
+
+def test_static_selection_spill_path(dev):
+    """More candidates than the top-k keeps in LDS (8192): a 640K context in blocks of 64 with 4
+    query heads, so the static call's scores spill into its scratch array (about 62 MB of the
+    64 MiB); the result equals the handle's selection bit for bit."""
+    w = gen.Workload("spill", 1, 4, 1, 64, 655360, 64, 512, 8, 16, 64, 4096, 512, 1, 8, 44)
+    gu.log(f"[no-alloc] spill n_tokens={w.n_tokens}")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, w.cluster)
+    dev_data = gu.upload(d, dev)
+    k_rep, sel_h, cnt_h, sc_h = _handle_selection(w, d, cs, dev_data)
+    s, e = cs[-2] * w.sub_chunk, min(cs[-1] * w.sub_chunk, w.n_tokens)    # the last cluster
+    lo = max(0, min(s, e - w.local_window))
+    n_cand = lo // w.block_size - (w.sink_tokens + w.block_size - 1) // w.block_size
+    assert n_cand > 8192                                                   # beyond the LDS rows
+    sel_s, cnt_s, sc_s = _static_selection(w, cs, dev_data[0], k_rep, 5)
+    assert np.array_equal(cnt_s, cnt_h)
+    assert np.array_equal(sel_s, sel_h)
+    assert np.array_equal(sc_s.view(np.uint32), sc_h.view(np.uint32))
