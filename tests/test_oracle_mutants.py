@@ -46,6 +46,16 @@ MUTANTS = [
      "float(scores[order[cnt - 2]] - scores[order[cnt - 1]])", [PINS]),
     ("causal_strict", "visible[:, n_fixed:] = pos[None, n_fixed:] <= rows[:, None]",
      "visible[:, n_fixed:] = pos[None, n_fixed:] < rows[:, None]", [PINS]),
+    ("rep_key_first_token", "        out[i] = keys.sum(axis=1) / n_valid\n", "        out[i] = keys[:, 0, :]\n", [PINS]),
+    ("fingerprint_sum", "    return rows.sum(axis=0) / (anchor_end - s)\n", "    return rows.sum(axis=0)\n", [PINS]),
+    ("attention_values_from_keys", "logical_rows(v_pages, block_table, pos, B),",
+     "logical_rows(k_pages, block_table, pos, B),", [PINS]),
+    ("attention_head_map_strided", "        g = (int(h) * Hkv) // Hq\n        Kg, Vg, visible = keys_of(g)",
+     "        g = int(h) % Hkv\n        Kg, Vg, visible = keys_of(g)", [PINS]),
+    ("attention_drops_sink", "fixed = np.concatenate([np.arange(geo.sink_eff * B), selected_positions",
+     "fixed = np.concatenate([np.arange(0), selected_positions", [PINS]),
+    ("attention_unnormalised", "out[:, hi, :] = (w @ Vg) / w.sum(axis=1, keepdims=True)",
+     "out[:, hi, :] = (w @ Vg) / w.shape[1]", [PINS]),
     ("softmax_not_per_head", "p = ex / ex.sum(axis=1, keepdims=True)", "p = ex / ex.sum()", [PINS]),
     ("attention_scale_1_over_d", "scale = 1.0 / math.sqrt(d) if", "scale = 1.0 / d if", [PINS]),
     ("partial_block_divisor", "        out[i] = keys.sum(axis=1) / n_valid",
