@@ -320,14 +320,27 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
     };
     auto mask_half = [&](int kb, f32x16& sc) {
       if constexpr (TOK) {
-        if (sel_rem != 0 && t == n_fixed - 1) {
-          const int lim = sel_rem - 16 * half;
+        // One branch for both masks: a local tile masks the keys after the row's own position, the
+        // last gathered tile its padding after the last selected row. A separate branch for the
+        // padding lets the compiler hoist its 16 lane masks into scalar registers, which spill,
+        // and splits the MFMA chains it sits between.
+        bool need = false;
+        int last = 0;   // last visible key of the tile, relative to the tile's first key
+        if (t >= n_fixed) {
+          const int key0 = local0 + (t - n_fixed) * kKeyTile;
+          need = key0 + kKeyTile > wave_p0;
+          last = p - key0;
+        } else if (sel_rem != 0 && t == n_fixed - 1) {
+          need = true;
+          last = sel_rem - 1;
+        }
+        if (need) {
+          const int lim = last - 16 * half;
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (32 * kb + e >= lim) sc[e] = -INFINITY;
+            if (32 * kb + e > lim) sc[e] = -INFINITY;
         }
-      }
-      if (t >= n_fixed) {
+      } else if (t >= n_fixed) {
         const int key0 = local0 + (t - n_fixed) * kKeyTile;
         if (key0 + kKeyTile > wave_p0) {
           const int lim = p - key0 - 16 * half;
