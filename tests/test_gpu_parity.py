@@ -108,13 +108,22 @@ def test_short_last_subchunk(dev):
     gu.check_output(res["out"], own["output"], "short tail")
 
 
-def test_bf16_output_is_rne_of_fp32(dev):
-    w, c = SHAPES["gqa128"]
-    gu.log("[parity] bf16 epilogue")
+@pytest.mark.parametrize("name,over", [
+    ("gqa128", {}),                                  # d 128, four heads per work-group
+    ("g7", {}),                                      # d 128, one head x 8 row blocks
+    ("g2d64", {}),                                   # d 64, 12-wave work-groups
+    ("gqa128", {"select_tokens": True, "top_k": 603}),   # token-level, padded last gathered tile
+    ("g5d64", {"select_tokens": True, "top_k": 200}),
+], ids=["gqa128", "g7", "g2d64", "gqa128-tokens", "g5d64-tokens"])
+def test_bf16_output_is_rne_of_fp32(dev, name, over):
+    """The bf16 epilogue of every kernel shape rounds the fp32 result to nearest even, bit for bit."""
+    w, c = SHAPES[name]
+    gu.log(f"[parity] bf16 epilogue {name} {over}")
     d = gen.make_layer(w)
     cs = gen.cluster_starts(w.n_sub_chunks, c)
-    r32 = gu.run_gpu(w, d, cs, dev)
-    r16 = gu.run_gpu(w, d, cs, dev, out_bf16=True)
+    r32 = gu.run_gpu(w, d, cs, dev, **over)
+    r16 = gu.run_gpu(w, d, cs, dev, out_bf16=True, **over)
+    assert np.array_equal(r16["sel_idx"], r32["sel_idx"])
     assert np.array_equal(r16["out"].view(np.uint16), gu.bf16_rne(r32["out"]))
 
 
@@ -135,6 +144,23 @@ def test_deterministic_and_page_permutation(dev):
     p = gu.run_gpu(w, dict(d, k_pages=kp, v_pages=vp, block_table=perm.astype(np.int32)), cs, dev)
     for key in ("k_rep", "sel_idx", "sel_cnt", "out", "scores"):
         assert np.array_equal(a[key], p[key]), key
+
+
+@pytest.mark.parametrize("over", [{}, {"select_tokens": True, "top_k": 333}], ids=["blocks", "tokens"])
+def test_null_block_table_is_identity(dev, over):
+    """A NULL block table maps logical block b to page b: bit-identical to passing the identity table
+    (representative keys, the token gather and attention all read pages through it)."""
+    w, c = SHAPES["g7"]
+    gu.log(f"[parity] NULL block table {over}")
+    d = gen.make_layer(w)
+    assert np.array_equal(d["block_table"], np.arange(w.n_blocks))
+    cs = gen.cluster_starts(w.n_sub_chunks, c)
+    a = gu.run_gpu(w, d, cs, dev, **over)
+    q, kp, vp, _ = gu.upload(d, dev)
+    b = gu.run_gpu(w, d, cs, dev, dev_data=(q, kp, vp, None), **over)
+    keys = ("sel_idx", "sel_cnt", "out", "scores") + (() if over else ("k_rep",))
+    for key in keys:
+        assert np.array_equal(a[key], b[key]), key
 
 
 def test_exact_ties_pick_lowest_index(dev):
