@@ -393,6 +393,32 @@ def test_abi_errors_on_device(dev):
         assert int(buf.abs().sum()) == 0
 
 
+def test_abi_selection_mode_mismatch(dev):
+    """The block-level selection call refuses a token-level handle and the token-level call a
+    block-level one, with SCALE_ERR_UNSUPPORTED, counting no call and launching nothing."""
+    import ctypes
+
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = gen.WORKLOADS["tiny"]
+    buf = torch.zeros(1 << 20, dtype=torch.int32, device=dev)
+    p = buf.data_ptr()
+    cs = np.array([0, 4, 8], dtype=np.int32)
+    n = ctypes.c_int64()
+    with pk.Scale(gu.config(w, 2, select_tokens=True)) as h:
+        assert pk.lib.scale_select_cluster(h.handle, p, 2048, p, cs.ctypes.data, 2, p, p, None) == \
+            pk.SCALE_ERR_UNSUPPORTED
+        assert pk.lib.scale_retrieval_calls(h.handle, ctypes.byref(n)) == 0 and n.value == 0
+    with pk.Scale(gu.config(w, 2)) as h:
+        assert pk.lib.scale_select_cluster_tokens(h.handle, p, 2048, p, None, cs.ctypes.data, 2, p, p, None) == \
+            pk.SCALE_ERR_UNSUPPORTED
+        assert pk.lib.scale_retrieval_calls(h.handle, ctypes.byref(n)) == 0 and n.value == 0
+    torch.cuda.synchronize()
+    assert int(buf.abs().sum()) == 0
+
+
 @pytest.mark.parametrize("name,w,cs", [
     # one block and one short sub-chunk: no candidates, no sinks, dense causal attention
     ("one_block", gen.WORKLOADS["tiny"].with_(n_tokens=64), [0, 1]),
