@@ -141,36 +141,40 @@ __global__ __launch_bounds__(kThreads) void block_logits_kernel(
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[i][q] = 0.0;
 
-  for (int d0 = 0; d0 < D; d0 += kLgDk) {
-    {
-      double vv[8];
-      float kk[kKeys][8];
+  // The global loads of slice d0 + kLgDk are issued before slice d0 is multiplied, so their
+  // latency hides under the fmas of the slice before.
+  double vv[8];
+  float kk[kKeys][8];
+  auto load_slice = [&](int d0) {
 #pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const double2 t = v_src ? *reinterpret_cast<const double2*>(v_src + d0 + e) : make_double2(0.0, 0.0);
-        vv[e] = t.x;
-        vv[e + 1] = t.y;
-      }
-#pragma unroll
-      for (int m = 0; m < kKeys; ++m)
-#pragma unroll
-        for (int e = 0; e < 8; e += 4) {
-          const float4 t = k_src ? *reinterpret_cast<const float4*>(k_src + m * D + d0 + e)
-                                 : make_float4(0.f, 0.f, 0.f, 0.f);
-          kk[m][e] = t.x;
-          kk[m][e + 1] = t.y;
-          kk[m][e + 2] = t.z;
-          kk[m][e + 3] = t.w;
-        }
-      __syncthreads();                                    // the previous slice has been read
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v_lds[ld_part + e][ld_row] = vv[e];
-#pragma unroll
-      for (int m = 0; m < kKeys; ++m)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) k_lds[m][ld_part + e][ld_row] = (double)kk[m][e];
-      __syncthreads();
+    for (int e = 0; e < 8; e += 2) {
+      const double2 t = v_src ? *reinterpret_cast<const double2*>(v_src + d0 + e) : make_double2(0.0, 0.0);
+      vv[e] = t.x;
+      vv[e + 1] = t.y;
     }
+#pragma unroll
+    for (int m = 0; m < kKeys; ++m)
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        const float4 t = k_src ? *reinterpret_cast<const float4*>(k_src + m * D + d0 + e)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+        kk[m][e] = t.x;
+        kk[m][e + 1] = t.y;
+        kk[m][e + 2] = t.z;
+        kk[m][e + 3] = t.w;
+      }
+  };
+  load_slice(0);
+  for (int d0 = 0; d0 < D; d0 += kLgDk) {
+    __syncthreads();                                      // the previous slice has been read
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v_lds[ld_part + e][ld_row] = vv[e];
+#pragma unroll
+    for (int m = 0; m < kKeys; ++m)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) k_lds[m][ld_part + e][ld_row] = (double)kk[m][e];
+    __syncthreads();
+    if (d0 + kLgDk < D) load_slice(d0 + kLgDk);
 #pragma unroll 4
     for (int dd = 0; dd < kLgDk; ++dd) {
       const double2 va = *reinterpret_cast<const double2*>(&v_lds[dd][4 * tr]);
@@ -235,6 +239,9 @@ constexpr int kVoteThreads = 1024;
 constexpr int kVoteWaves = kVoteThreads / 64;
 constexpr int kMaxLdsCand = 8192;        // scores of larger clusters live in the global spill row
 constexpr int kHistBins = 4096;          // radix digits of the first two passes (12 bits)
+constexpr int kFacLds = 2048;            // chunk factors (voting heads x chunks) kept in LDS
+constexpr int kStatsCached = 1;          // chunk statistics a lane holds in registers (64 chunks per head)
+constexpr int kWeightBatch = 8;          // weight loads in flight per candidate
 
 // Exclusive prefix sum over the work-group's threads in thread order; the total through *total.
 __device__ inline int block_exclusive_scan(int v, int* red, int* total) {
@@ -295,6 +302,7 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
   __shared__ int red_i[kVoteWaves];
   __shared__ unsigned hist[kHistBins];
   __shared__ int pick[2];
+  __shared__ double fac_lds[kTok ? 1 : kFacLds];
   const int row = blockIdx.x;
   const int sets = a.per_kv ? a.num_kv_heads : 1;
   const int j = row / sets;
@@ -318,40 +326,64 @@ __global__ __launch_bounds__(kVoteThreads) void vote_topk_kernel(VoteArgs a) {
     const int n_chunks = a.n_chunks;
     const int used = (n + kCandChunk - 1) / kCandChunk;
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    // the factors of the voting heads stay in LDS when they fit, else in the global scratch
+    const bool fac_in_lds = (h1 - h0) * used <= kFacLds;
     for (int h = h0 + wave; h < h1; h += kVoteWaves) {
       const int64_t hrow = (int64_t)j * num_q_heads + h;
       const double2* st = a.stats + hrow * n_chunks;
+      // a lane's first kStatsCached chunks k = lane + 64 u are loaded once, together
+      double2 sc[kStatsCached];
+#pragma unroll
+      for (int u = 0; u < kStatsCached; ++u)
+        sc[u] = lane + 64 * u < used ? st[lane + 64 * u] : make_double2(-DBL_MAX, 0.0);
       double m = -DBL_MAX;
-      for (int k = lane; k < used; k += 64) m = fmax(m, st[k].x);
+#pragma unroll
+      for (int u = 0; u < kStatsCached; ++u) m = fmax(m, sc[u].x);
+      for (int k = lane + 64 * kStatsCached; k < used; k += 64) m = fmax(m, st[k].x);
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) m = fmax(m, __shfl_xor(m, o, 64));
+      // the lane's chunks in increasing order, then the fixed butterfly
+      double e[kStatsCached];        // exp(m_k - M) of the cached chunks
+#pragma unroll
+      for (int u = 0; u < kStatsCached; ++u) e[u] = lane + 64 * u < used ? exp(sc[u].x - m) : 0.0;
       double sum = 0.0;
-      for (int k = lane; k < used; k += 64) sum += st[k].y * exp(st[k].x - m);
+#pragma unroll
+      for (int u = 0; u < kStatsCached; ++u)
+        if (lane + 64 * u < used) sum += sc[u].y * e[u];
+      for (int k = lane + 64 * kStatsCached; k < used; k += 64) sum += st[k].y * exp(st[k].x - m);
 #pragma unroll
       for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
       const double inv = 1.0 / sum;
-      double* f = a.factors + hrow * n_chunks;
-      for (int k = lane; k < used; k += 64) f[k] = exp(st[k].x - m) * inv;
+      double* f = fac_in_lds ? fac_lds + (h - h0) * used : a.factors + hrow * n_chunks;
+#pragma unroll
+      for (int u = 0; u < kStatsCached; ++u)
+        if (lane + 64 * u < used) f[lane + 64 * u] = e[u] * inv;
+      for (int k = lane + 64 * kStatsCached; k < used; k += 64) f[k] = exp(st[k].x - m) * inv;
     }
     __syncthreads();                                 // the factors are read by every thread below
     const double* wts = a.weights + (int64_t)j * num_q_heads * cand_stride;
-    const double* fac = a.factors + (int64_t)j * num_q_heads * n_chunks;
-    for (int c = threadIdx.x; c < n; c += kVoteThreads) {
-      const int k = c / kCandChunk;
-      double acc = 0.0;
-      int h = h0;
-      for (; h + 8 <= h1; h += 8) {
-        double wv[8], fv[8];
+    // per candidate: the sum over the voting heads, in head order, of weight x chunk factor
+    auto vote = [&](auto&& fac) {
+      for (int c = threadIdx.x; c < n; c += kVoteThreads) {
+        const int k = c / kCandChunk;
+        double acc = 0.0;
+        int h = h0;
+        for (; h + kWeightBatch <= h1; h += kWeightBatch) {
+          double wv[kWeightBatch];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          wv[u] = wts[(int64_t)(h + u) * cand_stride + c];
-          fv[u] = fac[(int64_t)(h + u) * n_chunks + k];
+          for (int u = 0; u < kWeightBatch; ++u) wv[u] = wts[(int64_t)(h + u) * cand_stride + c];
+#pragma unroll
+          for (int u = 0; u < kWeightBatch; ++u) acc = fma(wv[u], fac(h + u, k), acc);
         }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) acc = fma(wv[u], fv[u], acc);
+        for (; h < h1; ++h) acc = fma(wts[(int64_t)h * cand_stride + c], fac(h, k), acc);
+        score[c] = (float)acc;
       }
-      for (; h < h1; ++h) acc = fma(wts[(int64_t)h * cand_stride + c], fac[(int64_t)h * n_chunks + k], acc);
-      score[c] = (float)acc;
+    };
+    if (fac_in_lds) {
+      vote([&](int h, int k) { return fac_lds[(h - h0) * used + k]; });
+    } else {
+      const double* fac = a.factors + (int64_t)j * num_q_heads * n_chunks;
+      vote([&](int h, int k) { return fac[(int64_t)h * n_chunks + k]; });
     }
   }
   __syncthreads();
