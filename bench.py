@@ -354,7 +354,10 @@ def time_path(args, w, c, layers, dev, theta=None):
         step()
         n_warm += 1
         torch.cuda.synchronize()
-    h.enable_timing(True)
+    # Inside the timed region only the attention launches are bracketed by events (the roofline's
+    # launch time); an event pair around every stage would sit between launches that otherwise run
+    # back to back.
+    h.enable_stage_timing(("attention",))
     h.stage_times(reset=True)
     calls0 = h.retrieval_calls()
     torch.cuda.synchronize()
@@ -363,15 +366,20 @@ def time_path(args, w, c, layers, dev, theta=None):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    stages = h.stage_times(reset=True)
+    timed = h.stage_times(reset=True)
     calls = (h.retrieval_calls() - calls0) // max(args.steps, 1)
-    # per-launch spread: the same steps again, one at a time, outside the timed region
+    # the same steps again, one at a time, outside the timed region, every stage timed: the other
+    # stages' launch times and the per-launch spread of attention
+    h.enable_timing(True)
     per_step = []
+    stages = {k: (0.0, 0) for k in timed}
     for _ in range(args.steps):
         step()
         st = h.stage_times(reset=True)
         per_step.append(st["attention"][0] / max(st["attention"][1], 1))
+        stages = {k: (stages[k][0] + st[k][0], stages[k][1] + st[k][1]) for k in stages}
     per_step.sort()
+    stages["attention"] = timed["attention"]
     overlap = overlap_stats(h, bufs, w, layers[0], cs) if args.overlap and not tokens and not args.kv_sets else None
     h.close()
     del bufs

@@ -293,6 +293,13 @@ typedef enum {
  * on first use and recycled). */
 scale_status scale_enable_timing(scale_handle h, int enable);
 
+/* The same instrumentation for a subset of the stages: bit s of stage_mask (s a scale_stage)
+ * brackets stage s with a pair of events; 0 turns timing off. scale_enable_timing(h, e) is
+ * stage_mask = all stages for e != 0, none otherwise. Every event pair sits in the stream
+ * between two launches, so timing only the stages one needs keeps the others' launches back to
+ * back. SCALE_ERR_INVALID_ARG for bits at or above SCALE_NUM_STAGES. */
+scale_status scale_enable_stage_timing(scale_handle h, uint32_t stage_mask);
+
 /* Synchronises the handle's stream, then writes the accumulated device milliseconds and the
  * number of timed launches of each stage (arrays of SCALE_NUM_STAGES) since the last reset.
  * Either output may be NULL. reset != 0 zeroes the accumulators afterwards. */

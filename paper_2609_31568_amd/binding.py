@@ -29,7 +29,7 @@ EXPORTS = (
     "scale_init", "scale_free", "scale_rep_keys", "scale_select_cluster", "scale_sparse_prefill",
     "scale_status_string", "scale_retrieval_calls", "scale_cluster_geometry", "scale_enable_timing",
     "scale_stage_times", "scale_cluster_subchunks", "scale_rep_keys_range", "scale_select_cluster_tokens",
-    "scale_init_variant", "scale_fingerprints", "scale_select_cluster_static",
+    "scale_init_variant", "scale_fingerprints", "scale_select_cluster_static", "scale_enable_stage_timing",
 )
 STAGES = ("rep_keys", "fingerprint", "logits", "vote_topk", "attention", "cluster", "gather")
 
@@ -115,6 +115,8 @@ def _load():
     lib.scale_cluster_geometry.restype = ctypes.c_int
     lib.scale_enable_timing.argtypes = [vp, ctypes.c_int]
     lib.scale_enable_timing.restype = ctypes.c_int
+    lib.scale_enable_stage_timing.argtypes = [vp, ctypes.c_uint32]
+    lib.scale_enable_stage_timing.restype = ctypes.c_int
     lib.scale_stage_times.argtypes = [vp, vp, vp, ctypes.c_int]
     lib.scale_stage_times.restype = ctypes.c_int
     lib.scale_cluster_subchunks.argtypes = [vp, vp, i32, i32, ctypes.c_double, i32, i32, vp, vp, vp]
@@ -265,6 +267,13 @@ class Scale:
 
     def enable_timing(self, enable: bool = True):
         _check(lib.scale_enable_timing(self._h, 1 if enable else 0), "scale_enable_timing")
+
+    def enable_stage_timing(self, stages=()):
+        """Time only the named stages (names of STAGES); an empty selection turns timing off."""
+        mask = 0
+        for name in stages:
+            mask |= 1 << STAGES.index(name)
+        _check(lib.scale_enable_stage_timing(self._h, mask), "scale_enable_stage_timing")
 
     def stage_times(self, reset: bool = False) -> dict:
         """{stage: (device ms accumulated, launches)}; synchronises the handle's stream."""

@@ -17,7 +17,7 @@ struct ClusterGeo {
   int32_t sink_eff;  // sink blocks [0, sink_eff)
   int32_t n_cand;    // candidate blocks [sink_blk, sink_blk + n_cand)
   int32_t sel_cnt;   // min(top_k, n_cand)
-  int32_t pad;
+  int32_t item0;     // first attention work item of the cluster (host geometry; 0 where unused)
 };
 static_assert(sizeof(ClusterGeo) == 32, "ClusterGeo is uploaded as raw bytes");
 
@@ -134,6 +134,12 @@ hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, c
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
                                    const uint16_t* gv, int kpad, hipStream_t stream);
+
+// The attention work list of the clusters [0, n_clusters) written to `items` from their device
+// geometry: cluster j's items start at geo[j].item0; inside a cluster, position tiles from the last
+// to the first, each once per (head group, KV head), KV head fastest.
+hipError_t launch_build_work_items(const ClusterGeo* geo, int n_clusters, int tile_positions, int head_groups,
+                                   int num_kv_heads, WorkItem* items, hipStream_t stream);
 
 // Query positions per attention work item for a group of `group` query heads per KV head and a
 // head dim (a multiple of kTilePositions), and the number of head groups one KV head's query heads

@@ -75,12 +75,17 @@ struct scale_ctx {
   float* d_tok_score = nullptr;
   uint16_t* d_gk = nullptr;
   uint16_t* d_gv = nullptr;
+  // cluster geometry: the copy the device holds in d_geo (geo_dev_clusters entries; -1 when none) and
+  // a host scratch of max_clusters entries; items_valid when d_items holds the work list of d_geo
+  std::vector<ClusterGeo> geo_dev, geo_tmp;
+  int geo_dev_clusters = -1;
+  bool items_valid = false;
   // pinned staging ring
   size_t slot_bytes = 0;
   Slot slots[kRingSlots];
   int next_slot = 0;
-  // stage timing
-  bool timing = false;
+  // stage timing: bit s set = stage s bracketed by events
+  uint32_t timing_mask = 0;
   std::vector<TimedLaunch> timed;       // recorded, not yet read
   std::vector<hipEvent_t> spare_events; // recycled
   double stage_ms[SCALE_NUM_STAGES] = {};
@@ -113,6 +118,12 @@ scale_status validate_config(const scale_config* c, const scale_variant* v) {
   if (c->num_q_heads / c->num_kv_heads > 8) return SCALE_ERR_UNSUPPORTED;
   // sizes that keep every int32 index of the kernels in range
   if ((int64_t)c->max_tokens * c->num_q_heads * c->head_dim >= ((int64_t)1 << 40)) return SCALE_ERR_UNSUPPORTED;
+  {
+    // attention work items of the largest call (one per tile of positions, per head group and KV head)
+    const int group = c->num_q_heads / c->num_kv_heads;
+    const int64_t tiles = ((int64_t)c->max_tokens + kTilePositions - 1) / kTilePositions + c->max_clusters;
+    if (tiles * c->num_kv_heads * attention_head_groups(group, c->head_dim) >= INT32_MAX) return SCALE_ERR_UNSUPPORTED;
+  }
   if (v->select_tokens) {
     // gathered rows and token-scoring rows are int32 indices in the kernels
     const int64_t kpad = ((int64_t)c->top_k + scale::kTokenTile - 1) / scale::kTokenTile * scale::kTokenTile;
@@ -135,6 +146,10 @@ scale_status plan_geometry(const scale_config& c, const scale_variant& v, int32_
   if (!geo) return SCALE_OK;
   const int B = c.block_size;
   const int sink_blk = (c.sink_tokens + B - 1) / B;
+  const int group = c.num_q_heads / c.num_kv_heads;
+  const int tp = attention_tile_positions(group, c.head_dim);
+  const int64_t items_per_tile = (int64_t)attention_head_groups(group, c.head_dim) * c.num_kv_heads;
+  int64_t item0 = 0;
   for (int j = 0; j < n_clusters; ++j) {
     ClusterGeo& g = geo[j];
     g.s = (int32_t)((int64_t)cluster_start[j] * c.sub_chunk);
@@ -145,7 +160,9 @@ scale_status plan_geometry(const scale_config& c, const scale_variant& v, int32_
     g.sink_eff = std::min(sink_blk, g.lo_blk);
     g.n_cand = std::max(0, g.lo_blk - sink_blk) * (v.select_tokens ? B : 1);
     g.sel_cnt = std::min(c.top_k, g.n_cand);
-    g.pad = 0;
+    // capped: a cluster set whose work list exceeds the handle's capacity is refused before use
+    g.item0 = (int32_t)std::min<int64_t>(item0, INT32_MAX);
+    item0 += (int64_t)((g.e - g.s + tp - 1) / tp) * items_per_tile;
   }
   return SCALE_OK;
 }
@@ -174,13 +191,13 @@ hipEvent_t take_event(scale_ctx* h) {
 }
 
 // Opens / closes the timing bracket of one stage (no-ops unless timing is enabled).
-void stage_begin(scale_ctx* h) {
-  if (!h->timing) return;
+void stage_begin(scale_ctx* h, int stage) {
+  if (!(h->timing_mask >> stage & 1u)) return;
   h->open_start = take_event(h);
   if (h->open_start) (void)hipEventRecord(h->open_start, h->stream);
 }
 void stage_end(scale_ctx* h, int stage) {
-  if (!h->timing || !h->open_start) return;
+  if (!(h->timing_mask >> stage & 1u) || !h->open_start) return;
   hipEvent_t stop = take_event(h);
   if (stop && hipEventRecord(stop, h->stream) == hipSuccess) {
     h->timed.push_back({stage, h->open_start, stop});
@@ -246,6 +263,25 @@ scale_status upload(scale_ctx* h, Slot* s, void* dst, size_t bytes) {
 }
 
 scale_status check_launch(hipError_t e) { return e == hipSuccess ? SCALE_OK : SCALE_ERR_HIP; }
+
+// Makes d_geo hold geo[0, n_clusters): uploaded through a staging slot unless the device already
+// holds exactly these entries (the calls of one layer, and the layers of a prefill chunk, share
+// their clusters). Every call on the handle is ordered on its stream, so the host record of what
+// was last enqueued is what the device holds when the next launch runs.
+scale_status sync_geometry(scale_ctx* h, const ClusterGeo* geo, int n_clusters) {
+  const size_t bytes = sizeof(ClusterGeo) * (size_t)n_clusters;
+  if (n_clusters == h->geo_dev_clusters && std::memcmp(geo, h->geo_dev.data(), bytes) == 0) return SCALE_OK;
+  Slot* slot = nullptr;
+  scale_status st = acquire_slot(h, &slot);
+  if (st != SCALE_OK) return st;
+  std::memcpy(slot->host, geo, bytes);
+  h->geo_dev_clusters = -1;
+  h->items_valid = false;
+  if ((st = upload(h, slot, h->d_geo, bytes)) != SCALE_OK) return st;
+  std::memcpy(h->geo_dev.data(), geo, bytes);
+  h->geo_dev_clusters = n_clusters;
+  return SCALE_OK;
+}
 
 }  // namespace
 
@@ -346,7 +382,9 @@ scale_status scale_init_variant(const scale_config* cfg, const scale_variant* va
     release(h);
     return SCALE_ERR_OUT_OF_MEMORY;
   }
-  h->slot_bytes = std::max(sizeof(ClusterGeo) * mc + sizeof(WorkItem) * (size_t)h->max_items, (size_t)256);
+  h->slot_bytes = std::max(sizeof(ClusterGeo) * (size_t)mc, (size_t)256);
+  h->geo_dev.resize(mc);
+  h->geo_tmp.resize(mc);
   for (auto& s : h->slots) {
     if (hipHostMalloc(&s.host, h->slot_bytes, hipHostMallocDefault) != hipSuccess ||
         hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess) {
@@ -385,7 +423,7 @@ scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32
   const scale_config& c = h->cfg;
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_REP_KEYS);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, 0, n_tokens / c.block_size, c.num_kv_heads,
                                               c.block_size, c.head_dim, h->var.rep_kind == SCALE_REP_BOUNDS, k_rep,
                                               h->stream);
@@ -400,7 +438,7 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
   if (first_block > n_tokens / c.block_size) return SCALE_ERR_INVALID_ARG;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_REP_KEYS);
   const hipError_t e = scale::launch_rep_keys(k_pages, block_table, first_block, n_tokens / c.block_size,
                                               c.num_kv_heads, c.block_size, c.head_dim, h->var.rep_kind == SCALE_REP_BOUNDS,
                                               k_rep, h->stream);
@@ -418,31 +456,29 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
   scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
-  Slot* slot = nullptr;
-  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
-  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  ClusterGeo* geo = h->geo_tmp.data();
   plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
   int max_cand = 0;
   for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
-  if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
+  if ((st = sync_geometry(h, geo, n_clusters)) != SCALE_OK) return st;
 
   const int n_blocks = n_tokens / c.block_size;
   const int sink_blk = (c.sink_tokens + c.block_size - 1) / c.block_size;
   const double sigma = c.score_scale == 0.f ? 1.0 : (double)c.score_scale;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_FINGERPRINT);
   st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, h->d_fingerprints,
                                                h->d_fp64, h->stream));
   stage_end(h, SCALE_STAGE_FINGERPRINT);
   if (st != SCALE_OK) return st;
   h->last_clusters = n_clusters;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_LOGITS);
   st = check_launch(scale::launch_block_logits(h->d_fp64, k_rep, h->d_geo, n_clusters, max_cand, h->max_blocks,
                                                sink_blk, c.num_q_heads, c.num_kv_heads, c.head_dim,
                                                v.rep_kind == SCALE_REP_BOUNDS, sigma, h->d_weights, h->d_stats,
                                                h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_VOTE_TOPK);
   st = check_launch(scale::launch_vote_topk(h->d_weights, h->d_stats, h->d_factors, h->d_geo, n_clusters, max_cand,
                                             h->max_blocks, sink_blk, c.num_q_heads, c.num_kv_heads,
                                             v.kv_head_sets != 0, c.top_k, n_blocks, h->d_spill, sel_idx, sel_cnt,
@@ -463,31 +499,29 @@ scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int3
   scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
-  Slot* slot = nullptr;
-  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
-  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  ClusterGeo* geo = h->geo_tmp.data();
   plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
   int max_cand = 0;
   for (int j = 0; j < n_clusters; ++j) max_cand = std::max(max_cand, geo[j].n_cand);
-  if ((st = upload(h, slot, h->d_geo, sizeof(ClusterGeo) * n_clusters)) != SCALE_OK) return st;
+  if ((st = sync_geometry(h, geo, n_clusters)) != SCALE_OK) return st;
 
   const int first_token = (c.sink_tokens + c.block_size - 1) / c.block_size * c.block_size;
   const float sigma = c.score_scale == 0.f ? 1.0f : c.score_scale;
   float* fps = h->d_fingerprints;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_FINGERPRINT);
   st = check_launch(scale::launch_fingerprints(q, h->d_geo, n_clusters, c.num_q_heads, c.head_dim, fps, nullptr,
                                                h->stream));
   stage_end(h, SCALE_STAGE_FINGERPRINT);
   if (st != SCALE_OK) return st;
   h->last_clusters = n_clusters;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_LOGITS);
   st = check_launch(scale::launch_token_selection(fps, k_pages, block_table, h->d_geo, n_clusters, max_cand,
                                                   first_token, c.num_q_heads, c.num_kv_heads, c.head_dim,
                                                   c.block_size, sigma, h->tok_stride, h->d_tok_F, h->d_tok_stats,
                                                   h->d_tok_lse, h->d_tok_partial, h->stream));
   stage_end(h, SCALE_STAGE_LOGITS);
   if (st != SCALE_OK) return st;
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_VOTE_TOPK);
   st = check_launch(scale::launch_vote_topk_tokens(h->d_tok_partial, h->d_geo, n_clusters, h->tok_stride, max_cand,
                                                    first_token, c.num_kv_heads, v.kv_head_sets != 0, c.top_k,
                                                    n_tokens, h->d_tok_score, sel_idx, sel_cnt, scores_out,
@@ -520,7 +554,7 @@ scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t 
   const int32_t span = cluster_span(l_max, L, outer_subchunks, m);
   if (span > scale::kMaxClusterSpan) return SCALE_ERR_UNSUPPORTED;
 
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_CLUSTER);
   scale_status st = check_launch(scale::launch_subchunk_similarity(q, n_tokens, first_subchunk, L, c.num_q_heads,
                                                                    c.head_dim, span, h->d_sub_fp, h->d_inv_norm,
                                                                    h->d_band, h->stream));
@@ -564,56 +598,41 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
   scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);
   if (st != SCALE_OK) return st;
 
-  Slot* slot = nullptr;
-  if ((st = acquire_slot(h, &slot)) != SCALE_OK) return st;
-  ClusterGeo* geo = reinterpret_cast<ClusterGeo*>(slot->host);
+  ClusterGeo* geo = h->geo_tmp.data();
   plan_geometry(c, v, n_tokens, cluster_start, n_clusters, geo);
-  WorkItem* items = reinterpret_cast<WorkItem*>(geo + n_clusters);
 
-  // Work list. Clusters in order; inside a cluster, position tiles from the last (most keys) to
+  // Work list: clusters in order; inside a cluster, position tiles from the last (most keys) to
   // the first; each tile once per (head group, KV head), KV head fastest. Work-groups are handed to
   // the 8 XCDs round-robin, so a KV head stays on the same XCDs (and their L2) while the tiles of
-  // one cluster, which share the sink, selected and local K/V blocks, run together.
+  // one cluster, which share the sink, selected and local K/V blocks, run together. It is built on
+  // the device from the geometry, and again only when the geometry changes.
   const int B = c.block_size;
   const int group = c.num_q_heads / c.num_kv_heads;
   const int TP = scale::attention_tile_positions(group, c.head_dim);
   const int HG = scale::attention_head_groups(group, c.head_dim);
-  int64_t n_items = 0;
-  for (int j = 0; j < n_clusters; ++j)
-    n_items += (int64_t)((geo[j].e - geo[j].s + TP - 1) / TP) * c.num_kv_heads * HG;
+  const ClusterGeo& last = geo[n_clusters - 1];
+  const int64_t n_items = (int64_t)last.item0 + (int64_t)((last.e - last.s + TP - 1) / TP) * c.num_kv_heads * HG;
   if (n_items > h->max_items) return SCALE_ERR_CAPACITY;
-  int64_t k = 0;
-  for (int j = 0; j < n_clusters; ++j) {
-    const ClusterGeo& g = geo[j];
-    const int n_tiles = (g.e - g.s + TP - 1) / TP;
-    for (int t = n_tiles - 1; t >= 0; --t) {
-      const int p0 = g.s + t * TP;
-      const int nr = std::min(TP, g.e - p0);
-      for (int hg = 0; hg < HG; ++hg)
-        for (int kv = 0; kv < c.num_kv_heads; ++kv) items[k++] = {j, kv | (hg << 16), p0, nr};
-    }
+  if ((st = sync_geometry(h, geo, n_clusters)) != SCALE_OK) return st;
+  if (!h->items_valid) {
+    if ((st = check_launch(scale::launch_build_work_items(h->d_geo, n_clusters, TP, HG, c.num_kv_heads, h->d_items,
+                                                          h->stream))) != SCALE_OK)
+      return st;
+    h->items_valid = true;
   }
-
-  // geometry and items sit back to back in the slot; they go to two device buffers
-  if (hipMemcpyAsync(h->d_geo, geo, sizeof(ClusterGeo) * n_clusters, hipMemcpyHostToDevice, h->stream) != hipSuccess ||
-      hipMemcpyAsync(h->d_items, items, sizeof(WorkItem) * (size_t)n_items, hipMemcpyHostToDevice, h->stream) !=
-          hipSuccess ||
-      hipEventRecord(slot->done, h->stream) != hipSuccess)
-    return SCALE_ERR_HIP;
-  slot->pending = true;
 
   const float scale = c.softmax_scale == 0.f ? 1.0f / std::sqrt((float)c.head_dim) : c.softmax_scale;
   const float qk_scale_log2 = scale * 1.4426950408889634f;
   const bool tokens = v.select_tokens && h->kpad > 0;
   if (tokens) {
-    stage_begin(h);
+    stage_begin(h, SCALE_STAGE_GATHER);
     st = check_launch(scale::launch_gather_selected(k_pages, v_pages, block_table, sel_idx, sel_cnt,
                                                     v.kv_head_sets != 0, n_clusters, c.top_k, h->kpad, n_tokens,
                                                     c.num_kv_heads, c.head_dim, B, h->d_gk, h->d_gv, h->stream));
     stage_end(h, SCALE_STAGE_GATHER);
     if (st != SCALE_OK) return st;
   }
-  stage_begin(h);
+  stage_begin(h, SCALE_STAGE_ATTENTION);
   const hipError_t e = scale::launch_sparse_attention(
       q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, v.kv_head_sets != 0,
       c.top_k, c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
@@ -624,8 +643,12 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
 }
 
 scale_status scale_enable_timing(scale_handle h, int enable) {
-  if (!h) return SCALE_ERR_INVALID_ARG;
-  h->timing = enable != 0;
+  return scale_enable_stage_timing(h, enable ? (1u << SCALE_NUM_STAGES) - 1u : 0u);
+}
+
+scale_status scale_enable_stage_timing(scale_handle h, uint32_t stage_mask) {
+  if (!h || (stage_mask >> SCALE_NUM_STAGES) != 0) return SCALE_ERR_INVALID_ARG;
+  h->timing_mask = stage_mask;
   return SCALE_OK;
 }
 

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void geometry_kernel(GeoArgs a, ClusterGeo* __
   g.sink_eff = min(sink_blk, g.lo_blk);
   g.n_cand = max(0, g.lo_blk - sink_blk);
   g.sel_cnt = min(a.top_k, g.n_cand);
-  g.pad = 0;
+  g.item0 = 0;
   geo[a.first + i] = g;
 }
 

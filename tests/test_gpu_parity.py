@@ -127,6 +127,42 @@ def test_bf16_output_is_rne_of_fp32(dev, name, over):
     assert np.array_equal(r16["out"].view(np.uint16), gu.bf16_rne(r32["out"]))
 
 
+def test_cluster_sets_change_between_calls(dev):
+    """One handle, a sequence of layers whose clusters change, return and repeat (the handle keeps
+    the device geometry and work list of the last cluster set and uploads or rebuilds them only
+    when the set changes): every layer must give the bits of a fresh handle for its own set, and
+    the sets' calls must each select from the set they were given."""
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = SHAPES["gqa128"][0]
+    d = gen.make_layer(w)
+    q, kp, vp, bt = gu.upload(d, dev)
+    n_short = w.n_tokens - w.sub_chunk
+    cs_a = gen.cluster_starts(w.n_sub_chunks, 3)
+    cs_b = gen.cluster_starts(w.n_sub_chunks, 5)
+    cs_c = gen.cluster_starts(w.n_sub_chunks - 1, 3)     # the same starts as cs_a, one sub-chunk shorter
+    runs = [("a", cs_a, w.n_tokens), ("b", cs_b, w.n_tokens), ("a", cs_a, w.n_tokens), ("a", cs_a, w.n_tokens),
+            ("c", cs_c, n_short), ("a", cs_a, w.n_tokens)]
+    fresh = {}
+    for name, cs, n in runs:
+        if name not in fresh:
+            fresh[name] = gu.run_gpu(w, d, cs, dev, n_tokens=n, dev_data=(q[:n], kp, vp, bt))
+    cfg = gu.config(w, max(len(cs) - 1 for _, cs, _ in runs))
+    gu.log("[parity] cluster sets changing between calls on one handle")
+    with pk.Scale(cfg) as h:
+        for name, cs, n in runs:
+            bufs = pk.LayerBuffers(cfg, n, len(cs) - 1, device=dev, with_scores=True)
+            pk.run_layer(h, q[:n], kp, vp, bt, n, cs, bufs)
+            torch.cuda.synchronize()
+            ref = fresh[name]
+            assert np.array_equal(bufs.sel_cnt.cpu().numpy(), ref["sel_cnt"]), name
+            assert np.array_equal(bufs.sel_idx.cpu().numpy(), ref["sel_idx"]), name
+            assert np.array_equal(bufs.scores.cpu().numpy(), ref["scores"]), name
+            assert np.array_equal(bufs.out.cpu().numpy(), ref["out"]), name
+
+
 def test_deterministic_and_page_permutation(dev):
     w, c = SHAPES["g7"]
     gu.log("[parity] determinism + paging")
