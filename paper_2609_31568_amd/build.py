@@ -10,7 +10,7 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB_PATH = os.path.join(HERE, "libscale.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-KERNEL_SOURCES = ["rep_keys.hip", "select.hip", "select_tokens.hip", "sparse_attention.hip", "cluster.hip",
+KERNEL_SOURCES = ["rep_keys.hip", "select.hip", "select_tokens.hip", "sparse_attention.hip", "work_list.hip", "cluster.hip",
                   "static_select.hip"]
 HOST_SOURCES = ["scale_api.cpp"]
 
