@@ -20,7 +20,9 @@
  * Conventions shared by every call:
  *  - Plain C; no HIP or framework types. bf16 tensors are passed as uint16_t bit patterns.
  *  - Device pointers are caller-owned device allocations (any HIP allocation visible to the
- *    handle's device). The only host pointer is `cluster_start`.
+ *    handle's device). The only host pointer is `cluster_start`. q, k_pages, v_pages, k_rep and
+ *    out start at 16-byte-aligned addresses (every HIP allocation does; the kernels move 16 bytes
+ *    per lane): a call given another address returns SCALE_ERR_INVALID_ARG.
  *  - Every call validates all arguments on the host BEFORE any device work and returns a status;
  *    on error nothing is launched and no output is touched. Calls enqueue on the stream given to
  *    scale_init and return without synchronising; a kernel fault surfaces at the caller's next

@@ -264,6 +264,9 @@ scale_status upload(scale_ctx* h, Slot* s, void* dst, size_t bytes) {
 
 scale_status check_launch(hipError_t e) { return e == hipSuccess ? SCALE_OK : SCALE_ERR_HIP; }
 
+// The kernels move 16 bytes per lane through q, k_pages, v_pages, k_rep and out.
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 // Makes d_geo hold geo[0, n_clusters): uploaded through a staging slot unless the device already
 // holds exactly these entries (the calls of one layer, and the layers of a prefill chunk, share
 // their clusters). Every call on the handle is ordered on its stream, so the host record of what
@@ -419,7 +422,7 @@ scale_status scale_fingerprints(scale_handle h, float* fingerprints, int32_t n_c
 
 scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32_t* block_table, int32_t n_tokens,
                             float* k_rep) {
-  if (!h || !k_pages || !k_rep || n_tokens < 1) return SCALE_ERR_INVALID_ARG;
+  if (!h || !k_pages || !k_rep || n_tokens < 1 || !aligned16(k_pages)) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
@@ -433,7 +436,7 @@ scale_status scale_rep_keys(scale_handle h, const uint16_t* k_pages, const int32
 
 scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const int32_t* block_table,
                                   int32_t first_block, int32_t n_tokens, float* k_rep) {
-  if (!h || !k_pages || !k_rep || n_tokens < 1 || first_block < 0) return SCALE_ERR_INVALID_ARG;
+  if (!h || !k_pages || !k_rep || n_tokens < 1 || first_block < 0 || !aligned16(k_pages)) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   if (n_tokens % c.block_size) return SCALE_ERR_UNSUPPORTED;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
@@ -449,7 +452,7 @@ scale_status scale_rep_keys_range(scale_handle h, const uint16_t* k_pages, const
 scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_tokens, const float* k_rep,
                                   const int32_t* cluster_start, int32_t n_clusters, int32_t* sel_idx,
                                   int32_t* sel_cnt, float* scores_out) {
-  if (!h || !q || !k_rep || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
+  if (!h || !q || !k_rep || !sel_idx || !sel_cnt || !aligned16(q) || !aligned16(k_rep)) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   const scale_variant& v = h->var;
   if (v.select_tokens) return SCALE_ERR_UNSUPPORTED;
@@ -492,7 +495,7 @@ scale_status scale_select_cluster(scale_handle h, const uint16_t* q, int32_t n_t
 scale_status scale_select_cluster_tokens(scale_handle h, const uint16_t* q, int32_t n_tokens, const uint16_t* k_pages,
                                          const int32_t* block_table, const int32_t* cluster_start, int32_t n_clusters,
                                          int32_t* sel_idx, int32_t* sel_cnt, float* scores_out) {
-  if (!h || !q || !k_pages || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
+  if (!h || !q || !k_pages || !sel_idx || !sel_cnt || !aligned16(q) || !aligned16(k_pages)) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   const scale_variant& v = h->var;
   if (!v.select_tokens) return SCALE_ERR_UNSUPPORTED;
@@ -543,7 +546,7 @@ static int32_t cluster_span(int32_t l_max, int32_t sub_chunk, int32_t outer_subc
 scale_status scale_cluster_subchunks(scale_handle h, const uint16_t* q, int32_t n_tokens, int32_t first_subchunk,
                                      double theta, int32_t l_max, int32_t outer_subchunks, int32_t* cluster_start,
                                      int32_t* n_clusters, double* cos_band) {
-  if (!h || !q || !cluster_start || !n_clusters) return SCALE_ERR_INVALID_ARG;
+  if (!h || !q || !cluster_start || !n_clusters || !aligned16(q)) return SCALE_ERR_INVALID_ARG;
   if (n_tokens < 1 || std::isnan(theta) || l_max < 1 || outer_subchunks < 0) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   if (n_tokens > c.max_tokens) return SCALE_ERR_CAPACITY;
@@ -593,6 +596,7 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
                                   const int32_t* block_table, int32_t n_tokens, const int32_t* cluster_start,
                                   int32_t n_clusters, const int32_t* sel_idx, const int32_t* sel_cnt, void* out) {
   if (!h || !q || !k_pages || !v_pages || !sel_idx || !sel_cnt || !out) return SCALE_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(out)) return SCALE_ERR_INVALID_ARG;
   const scale_config& c = h->cfg;
   const scale_variant& v = h->var;
   scale_status st = plan_geometry(c, v, n_tokens, cluster_start, n_clusters, nullptr);

@@ -82,6 +82,7 @@ extern "C" scale_status scale_select_cluster_static(const scale_config* cfg, voi
   using namespace scale;
   // Host validation (the rules of scale_init and scale_select_cluster), before any HIP call.
   if (!q || !k_rep || !sel_idx || !sel_cnt) return SCALE_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k_rep)) & 15u) return SCALE_ERR_INVALID_ARG;
   const scale_variant v{};
   scale_status st = validate_config(cfg, &v);
   if (st != SCALE_OK) return st;

@@ -423,6 +423,24 @@ def test_abi_errors_on_device(dev):
             pk.SCALE_ERR_INVALID_ARG
         assert lib.scale_sparse_prefill(h.handle, p, p, p, None, 2048, cs.ctypes.data, 2, p, None, p) == \
             pk.SCALE_ERR_INVALID_ARG
+        # tensors that do not start on a 16-byte boundary (the kernels' vector width)
+        assert lib.scale_rep_keys(h.handle, p + 2, None, 2048, p) == pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_rep_keys_range(h.handle, p + 8, None, 0, 2048, p) == pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_select_cluster(h.handle, p + 2, 2048, p, cs.ctypes.data, 2, p, p, None) == \
+            pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_select_cluster(h.handle, p, 2048, p + 4, cs.ctypes.data, 2, p, p, None) == \
+            pk.SCALE_ERR_INVALID_ARG
+        for args in [(p + 2, p, p), (p, p + 2, p), (p, p, p + 2)]:
+            assert lib.scale_sparse_prefill(h.handle, *args, None, 2048, cs.ctypes.data, 2, p, p, p) == \
+                pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_sparse_prefill(h.handle, p, p, p, None, 2048, cs.ctypes.data, 2, p, p, p + 8) == \
+            pk.SCALE_ERR_INVALID_ARG
+        cs_out = np.zeros(9, dtype=np.int32)
+        n_cl = ctypes.c_int32()
+        assert lib.scale_cluster_subchunks(h.handle, p + 2, 2048, 0, 0.9, 1024, 0, cs_out.ctypes.data,
+                                           ctypes.byref(n_cl), None) == pk.SCALE_ERR_INVALID_ARG
+        assert lib.scale_select_cluster_static(ctypes.byref(cfg.base), None, p + 2, 2048, p, cs.ctypes.data, 2, p, p,
+                                               None) == pk.SCALE_ERR_INVALID_ARG
         n = ctypes.c_int64()
         assert lib.scale_retrieval_calls(h.handle, ctypes.byref(n)) == 0 and n.value == 0
         torch.cuda.synchronize()
