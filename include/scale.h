@@ -36,7 +36,10 @@
  *    q       bf16  [N][Hq][d]             token-major queries of the outer chunk
  *    k_pages bf16  [n_pages][Hkv][B][d]   paged key cache, one page = one block of B tokens
  *    v_pages bf16  [n_pages][Hkv][B][d]   paged value cache, same paging as k_pages
- *    block_table int32 [nb]               page holding logical block b; NULL = identity
+ *    block_table int32 [nb]               page holding logical block b; NULL = identity. The
+ *                                         kernels index a cache row as (page * Hkv + g) * B in
+ *                                         32 bits, so n_pages * Hkv * B < 2^31 (true of any K and
+ *                                         V page pools that fit in one device's memory together)
  *    k_rep   fp32  [nb][Hkv][d]           representative keys ([nb][Hkv][2][d]: channel-wise
  *                                         minimum, then maximum, with rep_kind = SCALE_REP_BOUNDS)
  *    sel_idx int32 [n_clusters][top_k]    selected blocks per cluster, ascending, -1 padded
