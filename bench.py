@@ -422,7 +422,11 @@ def time_path(args, w, c, layers, dev, theta=None):
                            "model); the kernel stages each k_rep tile once for up to 64 (cluster, head) rows, "
                            "so large cluster counts run above the HBM rate; fp64 FLOPs = 2 d per "
                            "(cluster, query head, candidate)"},
-        "vote_topk": {"GB/s": gbs(work["vote_bytes"], per_launch["vote_topk"]), "bytes": work["vote_bytes"]},
+        "vote_topk": {"GB/s": gbs(work["vote_bytes"], per_launch["vote_topk"]), "bytes": work["vote_bytes"],
+                      "bound": "latency",
+                      "note": "one work-group per output row: soft-voting sums, then three radix passes and an "
+                              "ordered compaction over the row's scores, each a handful of work-group barriers; "
+                              "a few MB per launch, so the launch time is latency, not bandwidth"},
         "peak_GB/s": PEAK_HBM_GBS,
     }
     shape = ("Llama-3-8B-shaped attention layer" if w.num_q_heads == 32 else "Qwen2-7B-shaped attention stack")
