@@ -127,13 +127,16 @@ hipError_t launch_gather_selected(const uint16_t* k_pages, const uint16_t* v_pag
 // Block-sparse attention over the work list. With gk != null (token-level selection) the selected
 // keys are the gathered rows gk / gv [cluster][Hkv][kpad][d], sel_cnt of them, instead of the
 // blocks sel_idx names. With `per_kv` the selection row of (cluster j, KV head g) is j * Hkv + g.
+// `queue` holds kAttentionQueues + 1 counters, zero before the launch and zero again after it (the
+// launch's persistent work-groups take their items from them).
 hipError_t launch_sparse_attention(const uint16_t* q, const uint16_t* k_pages, const uint16_t* v_pages,
                                    const int32_t* block_table, const ClusterGeo* geo,
                                    const WorkItem* items, int n_items, const int32_t* sel_idx,
                                    const int32_t* sel_cnt, bool per_kv, int top_k, int num_q_heads,
                                    int num_kv_heads, int head_dim, int block_size, int n_blocks,
                                    float qk_scale_log2, int out_bf16, void* out, const uint16_t* gk,
-                                   const uint16_t* gv, int kpad, hipStream_t stream);
+                                   const uint16_t* gv, int kpad, uint32_t* queue, hipStream_t stream);
+constexpr int kAttentionQueues = 8;
 
 // The attention work list of the clusters [0, n_clusters) written to `items` from their device
 // geometry: cluster j's items start at geo[j].item0; inside a cluster, position tiles from the last

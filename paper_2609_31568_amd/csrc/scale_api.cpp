@@ -49,6 +49,7 @@ struct scale_ctx {
   // device scratch
   ClusterGeo* d_geo = nullptr;
   WorkItem* d_items = nullptr;
+  uint32_t* d_attn_queue = nullptr;   // attention work-queue counters (zero between launches)
   float* d_fingerprints = nullptr;
   // block-level selection: fp64 fingerprints, per-chunk weights and softmax partials, chunk factors
   double* d_fp64 = nullptr;
@@ -221,6 +222,7 @@ void release(scale_ctx* h) {
   }
   (void)hipFree(h->d_geo);
   (void)hipFree(h->d_items);
+  (void)hipFree(h->d_attn_queue);
   (void)hipFree(h->d_fingerprints);
   (void)hipFree(h->d_fp64);
   (void)hipFree(h->d_weights);
@@ -354,6 +356,8 @@ scale_status scale_init_variant(const scale_config* cfg, const scale_variant* va
   const bool blocks = !v.select_tokens;
   bool ok = dev((void**)&h->d_geo, sizeof(ClusterGeo) * mc) &&
             dev((void**)&h->d_items, sizeof(WorkItem) * (size_t)h->max_items) &&
+            dev((void**)&h->d_attn_queue, sizeof(uint32_t) * (scale::kAttentionQueues + 1)) &&
+            hipMemset(h->d_attn_queue, 0, sizeof(uint32_t) * (scale::kAttentionQueues + 1)) == hipSuccess &&
             dev((void**)&h->d_fingerprints, sizeof(float) * mc * row_elems) &&
             dev((void**)&h->d_fp64, blocks ? sizeof(double) * mc * row_elems : 0) &&
             dev((void**)&h->d_weights, blocks ? sizeof(double) * mc * c.num_q_heads * (int64_t)h->max_blocks : 0) &&
@@ -641,7 +645,7 @@ scale_status scale_sparse_prefill(scale_handle h, const uint16_t* q, const uint1
       q, k_pages, v_pages, block_table, h->d_geo, h->d_items, (int)n_items, sel_idx, sel_cnt, v.kv_head_sets != 0,
       c.top_k, c.num_q_heads, c.num_kv_heads, c.head_dim, B, n_tokens / B, qk_scale_log2,
       c.out_dtype == SCALE_OUT_BF16, out, tokens ? h->d_gk : nullptr, tokens ? h->d_gv : nullptr, h->kpad,
-      h->stream);
+      h->d_attn_queue, h->stream);
   stage_end(h, SCALE_STAGE_ATTENTION);
   return check_launch(e);
 }

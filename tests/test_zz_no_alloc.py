@@ -72,8 +72,9 @@ def test_static_selection_equals_handle_selection(dev):
     w = gen.WORKLOADS["stress1m"]
     cs = gen.cluster_starts(w.n_sub_chunks, 1)
     cfg = gu.config(w, len(cs) - 1)
+    fake = 256   # an aligned address that the refused call never dereferences
     with pytest.raises(pk.ScaleError) as e:
-        pk.scale_select_cluster_static(cfg, 1, w.n_tokens, 1, cs, 1, 1, None)
+        pk.scale_select_cluster_static(cfg, fake, w.n_tokens, fake, cs, fake, fake, None)
     assert e.value.status == pk.SCALE_ERR_CAPACITY
 
 
