@@ -200,7 +200,17 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
   // item precede its reuse.
   __shared__ int item_slot[2];
   const int queue_id = blockIdx.x & (kQueues - 1);
-  auto take = [&]() { return queue_id + kQueues * (int)atomicAdd(&queue[queue_id], 1u); };
+  // A take tries the work-group's own queue first and, once that is empty, the others in turn, so
+  // CUs of a faster XCD finish the items a slower XCD has left (the stolen items lose their L2
+  // locality, which only the last items of a launch pay); n_items when every queue is empty.
+  auto take = [&]() {
+    for (int i = 0; i < kQueues; ++i) {
+      const int qq = (queue_id + i) & (kQueues - 1);
+      const int v = qq + kQueues * (int)atomicAdd(&queue[qq], 1u);
+      if (v < n_items) return v;
+    }
+    return n_items;
+  };
   if (threadIdx.x == 0) item_slot[0] = take();
   __syncthreads();
   int cur_item = item_slot[0];
