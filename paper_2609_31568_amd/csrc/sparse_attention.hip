@@ -192,8 +192,9 @@ __global__ __launch_bounds__(GH * RB * 64) void sparse_attention_kernel(
   // Persistent work-groups: work-group b serves queue b % kQueues (with the hardware's round-robin
   // placement, one queue per XCD), taking the items b % kQueues, + kQueues, + 2 kQueues, ... of the
   // work list in order from the queue's counter until they run out. A work-group runs item after
-  // item without leaving the CU, so no item waits for the launch of a new work-group, and the
-  // queues balance the CUs to within one item.
+  // item without leaving the CU, so no item waits for the launch of a new work-group; a queue
+  // balances the CUs that serve it to within one item, and taking from the other queues once its
+  // own is empty (below) balances the XCDs.
   // Each item's successor is taken from the queue when the item starts and published at the end of
   // its prologue, so the atomic's latency hides under the prologue's loads; the two slots
   // alternate, and every wave reads a slot (at the end of an item) before the barriers of the next
