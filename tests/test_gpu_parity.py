@@ -163,6 +163,41 @@ def test_cluster_sets_change_between_calls(dev):
             assert np.array_equal(bufs.out.cpu().numpy(), ref["out"]), name
 
 
+def test_work_item_counts_alternate_on_one_handle(dev):
+    """Attention work-groups take their items from per-XCD queues whose counters the last
+    work-group clears for the next launch. Alternate launches with fewer items than the eight
+    queues, as many, a few more and many on one handle: every launch must give the bits of a fresh
+    handle, so no counter is left set and no item is skipped or taken twice."""
+    import torch
+
+    import paper_2609_31568_amd as pk
+
+    w = SHAPES["gqa128"][0]     # d 128, 2 KV heads of 4 query heads: 64-row items per KV head
+    d = gen.make_layer(w)
+    q, kp, vp, bt = gu.upload(d, dev)
+    full = gen.cluster_starts(w.n_sub_chunks, 3)
+    # (context length, cluster starts): 128 tokens -> 2 row tiles x 2 KV heads = 4 items; 256 -> 8;
+    # 384 -> 12; the full context -> 256 items
+    runs = [(128, [0, 1]), (w.n_tokens, full), (256, [0, 1]), (384, [0, 1]), (w.n_tokens, full), (128, [0, 1])]
+    fresh = {}
+    for n, cs in runs:
+        if n not in fresh:
+            fresh[n] = gu.run_gpu(w, d, np.asarray(cs, dtype=np.int32), dev, n_tokens=n,
+                                  dev_data=(q[:n], kp, vp, bt))
+    cfg = gu.config(w, len(full) - 1)
+    gu.log("[parity] work-item counts alternating on one handle")
+    with pk.Scale(cfg) as h:
+        for n, cs in runs:
+            cs = np.asarray(cs, dtype=np.int32)
+            bufs = pk.LayerBuffers(cfg, n, len(cs) - 1, device=dev, with_scores=True)
+            pk.run_layer(h, q[:n], kp, vp, bt, n, cs, bufs)
+            torch.cuda.synchronize()
+            assert np.array_equal(bufs.out.float().cpu().numpy(), fresh[n]["out"]), n
+    for n in (128, 384):
+        ref = _oracle(w, d, np.asarray([0, 1], dtype=np.int32), n=n)
+        gu.check_output(fresh[n]["out"], ref["output"], f"{n}-token context")
+
+
 def test_deterministic_and_page_permutation(dev):
     w, c = SHAPES["g7"]
     gu.log("[parity] determinism + paging")
