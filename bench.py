@@ -429,7 +429,9 @@ def time_path(args, w, c, layers, dev, theta=None):
                               "a few MB per launch, so the launch time is latency, not bandwidth"},
         "peak_GB/s": PEAK_HBM_GBS,
     }
-    shape = ("Llama-3-8B-shaped attention layer" if w.num_q_heads == 32 else "Qwen2-7B-shaped attention stack")
+    shape = {32: "Llama-3-8B-shaped attention layer", 28: "Qwen2-7B-shaped attention stack",
+             8: "four-way KV-head shard (8 query / 2 KV heads) of a Llama-3-8B-shaped attention layer"}.get(
+                 w.num_q_heads, f"{w.num_q_heads} query / {w.num_kv_heads} KV head attention layer")
     return {
         "metric": METRIC,
         "value": round(tokens_per_s, 1),

@@ -106,6 +106,10 @@ WORKLOADS = {
     "llama32k": Workload("llama32k", 1, 32, 8, 128, 32768, 128, 512, 8, 16, 128, 4096, 64, 2, 8, 1),
     # same layer at 128K context: the headline workload
     "llama128k": Workload("llama128k", 1, 32, 8, 128, 131072, 128, 512, 8, 32, 128, 4096, 256, 2, 16, 2),
+    # one GPU's share of the 128K layer split four ways by KV head (8q / 2kv): the attention shape
+    # of one shard; its selection votes over its own 8 heads (the cross-shard score sum is the one
+    # exchange of the split and is not run here)
+    "llama128k_tp4": Workload("llama128k_tp4", 1, 8, 2, 128, 131072, 128, 512, 8, 32, 128, 4096, 256, 2, 16, 6),
     # Qwen2-7B-shaped stack (28 layers, 28q / 4kv, d 128), 256K context
     "qwen256k": Workload("qwen256k", 28, 28, 4, 128, 262144, 128, 1024, 4, 32, 128, 8192, 512, 1, 8, 3),
     # Llama-3-8B layer at 1M context; the cluster size is swept over {1, 2, 4, 8, 16}

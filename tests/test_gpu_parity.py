@@ -415,6 +415,18 @@ def test_qwen256k_layer_sampled(dev, layer, seed):
     _sampled_layer(dev, w, d, cs, clusters, rng, f"qwen256k layer {layer}")
 
 
+def test_kv_head_shard_sampled(dev):
+    """The 128K layer's four-way KV-head shard (8 query / 2 KV heads per GPU): 4096 work items,
+    16 per CU, so the queues run dry four times sooner than at the full layer."""
+    w = gen.WORKLOADS["llama128k_tp4"]
+    gu.log("[parity] llama128k_tp4: generating")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, w.cluster)
+    rng = np.random.default_rng(16)
+    clusters = _sample_clusters(len(cs) - 1, 10, rng)
+    _sampled_layer(dev, w, d, cs, clusters, rng, "llama128k_tp4")
+
+
 def test_topk_spill_path(dev):
     """More candidates than the top-k keeps in LDS (8192): a 640K context in blocks of 64 gives up to
     10175 candidates, so the last clusters' scores go through the global spill row, and their heads'
