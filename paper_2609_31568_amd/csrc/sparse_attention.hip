@@ -14,6 +14,10 @@
 // (cluster, KV head); their tiles are marked by negative table entries, and the padding rows of a
 // partial last gathered tile are masked like the causal mask.
 //
+// The launch is persistent: one work-group per CU runs item after item, taking them in work-list
+// order from eight queue counters (one per XCD, the others once its own is empty), so no item
+// waits for a work-group launch and the CUs end within about one item of each other.
+//
 // Per 64-key tile and wave (d = head dim, 32 query rows of one head):
 //   S^T = K Q^T     v_mfma_f32_32x32x16_bf16, A = K rows from LDS, B = Q held in registers
 //   online softmax  fp32 in base 2 with the softmax scale folded into one fma per score. A
