@@ -217,6 +217,55 @@ def test_token_full_size(dev, name, c):
             gu.log(f"[tokens] {name}: clusters up to {j} every row, worst max-abs {worst[0]:.2e} rel-L2 {worst[1]:.2e}")
 
 
+def test_token_128k_one_call_per_subchunk_sampled(dev):
+    """Token-level selection on the 128K layer with clusters of one sub-chunk (256 selection calls,
+    the c = 1 end of the token sweep): the GPU runs the whole layer; 12 sampled clusters are checked
+    against the oracle (fingerprints, scores, selection) and their first, last and two random
+    32-row tiles of attention output under the GPU's selection."""
+    w = gen.WORKLOADS["llama128k"].with_(cluster=1)
+    k = 32 * w.block_size
+    B = w.block_size
+    gu.log("[tokens] llama128k c=1: generating")
+    d = gen.make_layer(w)
+    cs = gen.cluster_starts(w.n_sub_chunks, 1)
+    J = len(cs) - 1
+    geo = oracle.geometry(w.n_tokens, w.sub_chunk, B, w.sink_tokens, w.local_window, k, cs, select_tokens=True)
+    rng = np.random.default_rng(17)
+    clusters = sorted({0, J - 1, *(int(x) for x in rng.choice(np.arange(1, J - 1), size=10, replace=False))})
+    rows = gu.sample_rows([geo[j] for j in clusters], rng, tiles_per_cluster=2)
+    gu.log(f"[tokens] llama128k c=1: GPU, {J} clusters")
+    res = _run(w, d, cs, dev, k, out_rows=np.concatenate(rows))
+    assert res["calls"] == J
+    n_max = max(geo[j].sink_blk * B + geo[j].n_cand for j in clusters)
+    K_all = oracle.logical_rows(d["k_pages"], d["block_table"], np.arange(n_max), B)
+    ref = {"geometry": [], "fingerprints": [], "scores": [], "selections": []}
+    cands = []
+    for j in clusters:
+        g = geo[j]
+        v = oracle.anchor_fingerprint(d["q"], g.s, g.anchor_end)
+        cand = K_all[g.sink_blk * B:g.sink_blk * B + g.n_cand]
+        sc = oracle.soft_vote(oracle.block_logits(v, cand, w.num_kv_heads))
+        sel, _ = oracle.select_topk(sc, g.sink_blk * B, k)
+        for key, val in (("geometry", g), ("fingerprints", v), ("scores", sc), ("selections", sel)):
+            ref[key].append(val)
+        cands.append(cand)
+    gu.log(f"[tokens] llama128k c=1: oracle selection of {len(clusters)} clusters")
+    bounds = gu.token_score_bounds(ref, cands, w.num_kv_heads)
+    del cands, K_all
+    gu.check_rounding(res["fingerprints"][clusters], np.stack(ref["fingerprints"]), "fingerprints")
+    worst = gu.check_token_scores(res["scores"][clusters], ref, bounds, B, "llama128k c=1")
+    n_exact = gu.check_token_selection(res["sel_idx"][clusters], res["sel_cnt"][clusters], res["scores"][clusters],
+                                       ref, bounds, B, "llama128k c=1")
+    gu.log(f"[tokens] llama128k c=1: worst relative score error {worst:.2e}; {n_exact} of {len(clusters)} sampled "
+           f"clusters above the margin")
+    sels = gu.gpu_selections(res, J)
+    at = 0
+    for i, j in enumerate(clusters):
+        o_ref = oracle.attention_rows(d["q"], d["k_pages"], d["v_pages"], d["block_table"], geo[j], sels[j], rows[i], B)
+        gu.check_output(res["out"][at:at + len(rows[i])], o_ref, f"llama128k c=1 cluster {j}")
+        at += len(rows[i])
+
+
 def test_token_short_last_subchunk(dev):
     """n_tokens = 2368: nine sub-chunks of 256 and a last one of 64; clusters of 4; a budget off the
     tile."""
