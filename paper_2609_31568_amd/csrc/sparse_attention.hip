@@ -515,12 +515,12 @@ struct LaunchArgs {
 // shape here), at least one per queue that holds an item, never more than there are items.
 template <class K>
 int persistent_grid(K kernel, int threads, int n_items) {
-  static int per_cu = -1;   // the kernel's resident work-groups per CU (same for every gfx950 device)
-  if (per_cu < 0) {
+  // the kernel's resident work-groups per CU (the same on every gfx950 device), found once
+  // (initialisation of a local static is thread-safe)
+  static const int per_cu = [&]() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
-    per_cu = n;
-  }
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) == hipSuccess && n >= 1 ? n : 1;
+  }();
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
                                               hipSuccess || cus < 1)
